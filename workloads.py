@@ -1,0 +1,113 @@
+"""Seeded synthetic workloads shaped like the serving workloads of the paper.
+
+Holds no attention arithmetic: only the shapes, the seeded draws and the row samples that both the
+oracle side and the HIP side of a test or benchmark receive.  The paper measures on production
+traces and trained video models that are not available; these tensors stand in for the attention
+inputs of such a model:
+  * 32760 tokens = 21 latent frames x 30 x 52 (a 480p-class latent after 2x2 patchify),
+    75600 tokens = 21 x 45 x 80 (720p-class); tokens are flattened frame-major.
+  * 12 and 40 heads of width 128: a ~1.3B-class and a large video DiT.
+  * The packed case is one coalesced chunk batch of six sessions (paper Sec. 3.1).
+  * Q, V ~ N(0, 1); K ~ N(0, 1) plus, for the DiT shapes, one offset per (head, channel) drawn
+    from N(0, 2) (variance 2) to mimic channel outliers.  Draws are float32 from one CPU
+    torch.Generator seeded with the workload number, in the order q, k, v, offset, then rounded
+    once to bfloat16 (round to nearest even): both sides get these same bf16 values.
+"""
+import hashlib
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    seqlens: tuple          # tokens of each segment (one entry = a dense sequence)
+    H: int
+    d: int
+    seed: int
+    k_offset: bool = False  # add a per-(head, channel) N(0, 2) offset to K
+    note: str = field(default="", compare=False)
+
+    @property
+    def T(self):
+        return int(sum(self.seqlens))
+
+    @property
+    def cu_seqlens(self):
+        return np.concatenate([[0], np.cumsum(self.seqlens)]).astype(np.int32)
+
+    @property
+    def max_seqlen(self):
+        return int(max(self.seqlens)) if self.seqlens else 0
+
+    @property
+    def flops(self):
+        """Algorithmic flops of one call: sum_s 4 L_s^2 d H (QK^T and PV, 2 flops per MAC)."""
+        return sum(4 * int(L) ** 2 * self.d * self.H for L in self.seqlens)
+
+    @property
+    def hbm_bytes(self):
+        """Algorithmic HBM bytes of one call: Q, K, V read once and O written once, bf16."""
+        return 4 * self.T * self.H * self.d * 2
+
+    @property
+    def scale(self):
+        return float(np.float32(1.0) / np.sqrt(np.float32(self.d)))
+
+
+WORKLOADS = {
+    "tiny": Workload("tiny", (1024,), 2, 64, 1, note="4x16x16 latent grid, L=1024, H=2, d=64"),
+    "dit_small": Workload("dit_small", (32760,), 12, 128, 2, True,
+                          note="21x30x52 latent, L=32760, H=12, d=128"),
+    "dit_large": Workload("dit_large", (32760,), 40, 128, 3, True,
+                          note="21x30x52 latent, L=32760, H=40, d=128"),
+    "highres": Workload("highres", (75600,), 40, 128, 4, True,
+                        note="21x45x80 latent, L=75600, H=40, d=128"),
+    "varlen_serving": Workload("varlen_serving", (8190, 8190, 16380, 32760, 32760, 2730), 12,
+                               128, 5, note="6 packed sessions, T=101010, H=12, d=128"),
+}
+ORDER = ["tiny", "dit_small", "dit_large", "highres", "varlen_serving"]
+
+
+def make_inputs(w, seed=None):
+    """(q, k, v) as bf16 CPU tensors [T, H, d], drawn as described in the module docstring."""
+    g = torch.Generator().manual_seed(w.seed if seed is None else seed)
+    shape = (w.T, w.H, w.d)
+    q = torch.randn(shape, generator=g, dtype=torch.float32).to(torch.bfloat16)
+    k32 = torch.randn(shape, generator=g, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, dtype=torch.float32).to(torch.bfloat16)
+    if w.k_offset:
+        offset = torch.randn((w.H, w.d), generator=g, dtype=torch.float32) * float(np.sqrt(2.0))
+        k32 += offset
+    k = k32.to(torch.bfloat16)
+    del k32
+    return q, k, v
+
+
+def bf16_bits(t):
+    """numpy uint16 view of a bf16 CPU tensor's bit patterns (what the oracle reads)."""
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def sha256(t):
+    return hashlib.sha256(bf16_bits(t).tobytes()).hexdigest()
+
+
+def sample_rows(w, n_random=64, seed=None):
+    """(row_t, row_h): for every head, the first and last token of every non-empty segment plus
+    n_random seeded random tokens per segment (seed 100 + workload seed)."""
+    rng = np.random.default_rng(100 + w.seed if seed is None else seed)
+    cu = w.cu_seqlens
+    ts = []
+    for s in range(len(w.seqlens)):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        if hi <= lo:
+            continue
+        ts.extend([lo, hi - 1])
+        ts.extend(rng.integers(lo, hi, size=n_random).tolist())
+    ts = np.asarray(ts, dtype=np.int64)
+    row_t = np.tile(ts, w.H)
+    row_h = np.repeat(np.arange(w.H, dtype=np.int32), ts.size)
+    return row_t, row_h
