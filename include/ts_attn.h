@@ -1,0 +1,107 @@
+/*
+ * ts_attn.h -- C ABI of the MI355X (gfx950) fused attention library libts_attn.so.
+ *
+ * The operation.  The paper's serving runtime runs one model call per coalesced chunk batch:
+ * the ready sessions on a GPU are packed together and the model is invoked once for all of
+ * them (Sec. 3.1, "Concurrent chunk execution"); every session keeps its own isolated state
+ * region (Sec. 6.1, "Session memory layout").  The dominant per-step cost of such a call in a
+ * video diffusion transformer is multi-head self-attention over the flattened
+ * frames x height x width latent tokens, whose cost grows quadratically with the number of
+ * tokens (Sec. 1).  In a packed batch each session attends only to its own tokens, so the
+ * batch is a list of segments and attention is block-diagonal:
+ *
+ *   for segment s = tokens [cu[s], cu[s+1]), token t in s, head h, channel c:
+ *     O[t,h,c] = sum_j softmax_j(scale * <Q[t,h,:], K[j,h,:]>) * V[j,h,c],  j over segment s,
+ *
+ * non-causal (j ranges over the whole segment).  The library computes this in one fused
+ * kernel: Q K^T, an online softmax and P V on bf16 matrix cores with fp32 accumulation.
+ *
+ * Common conventions of every entry point
+ *  - Tensors q, k, v, o: device pointers to bfloat16, contiguous, token-major [T][H][d]
+ *    (row stride H*d elements).  For the dense call T = B*L, i.e. [B][L][H][d].
+ *    Base pointers must be 16-byte aligned.  d must be 64 or 128.
+ *  - o must not overlap q, k or v (they may overlap each other).
+ *  - scale: any finite float (0 is allowed: O becomes the segment mean of V).  Typical:
+ *    1/sqrt(d) rounded to float.
+ *  - stream: a hipStream_t passed as void* (NULL = the legacy default stream).  Calls are
+ *    asynchronous: they enqueue work on stream and return without synchronizing.  Buffers
+ *    must stay valid until that work completes.  Device faults surface at the caller's next
+ *    synchronization.
+ *  - Ownership: the caller owns every buffer; the library keeps no pointer after returning.
+ *  - Errors: argument checks run on the host before any HIP call and return a ts_status
+ *    without touching the device.  Empty problems (B, L, T or nseq equal to 0) are no-ops
+ *    returning TS_OK.  A device that is not gfx950 gives TS_ERR_UNSUPPORTED.
+ *  - Determinism: results are bitwise reproducible for fixed inputs on one device (no atomics
+ *    in the arithmetic, fixed reduction order), and a row's result does not depend on the
+ *    other segments of the batch.
+ *  - Thread safety: all entry points may be called concurrently from several host threads.
+ *  - Size limits: (L or max_seqlen + 256) * H * d * 2 bytes must stay below 2^31, and the
+ *    work items (H * ceil(L / 256) per sequence; H * (ceil(T / 256) + nseq) for packed
+ *    batches) below 2^23.  Larger problems return TS_ERR_SHAPE.
+ */
+#ifndef TS_ATTN_H
+#define TS_ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TS_ATTN_ABI_VERSION 1
+
+typedef enum ts_status {
+  TS_OK = 0,
+  TS_ERR_NULL = 1,        /* a required pointer is NULL */
+  TS_ERR_SHAPE = 2,       /* negative or inconsistent sizes, or above the size limit */
+  TS_ERR_HEAD_DIM = 3,    /* d is not 64 or 128 */
+  TS_ERR_SCALE = 4,       /* scale is NaN or infinite */
+  TS_ERR_ALIGN = 5,       /* a tensor pointer is not 16-byte aligned */
+  TS_ERR_ALIAS = 6,       /* o overlaps q, k or v */
+  TS_ERR_UNSUPPORTED = 7, /* no usable gfx950 device */
+  TS_ERR_HIP = 8,         /* a HIP runtime call or kernel launch failed */
+  TS_ERR_NOMEM = 9,       /* device scratch allocation failed */
+  TS_ERR_SEGMENTS = 10    /* cu_seqlens contents invalid (reported only in validation mode) */
+} ts_status;
+
+/*
+ * Dense batch: B independent sequences of L tokens each; q, k, v, o are [B][L][H][d] bf16.
+ * Every sequence is one segment; the result equals ts_attn_fwd_varlen with
+ * cu_seqlens = {0, L, 2L, ..., B*L}, bit for bit.
+ * Returns TS_OK when the work was enqueued on stream.
+ */
+int ts_attn_fwd(const void* q, const void* k, const void* v, void* o, int32_t B, int32_t L,
+                int32_t H, int32_t d, float scale, void* stream);
+
+/*
+ * Packed variable-length batch (one coalesced chunk batch of the paper's Sec. 3.1):
+ * q, k, v, o are [T][H][d] bf16 with T = total_tokens.
+ *  cu_seqlens  DEVICE pointer to nseq+1 int32 offsets: cu[0] = 0, nondecreasing,
+ *              cu[nseq] = total_tokens.  Segment s is tokens [cu[s], cu[s+1]); empty
+ *              segments are allowed.  Every segment length must be <= max_seqlen.
+ *  nseq        number of segments (host value).
+ *  max_seqlen  an upper bound of every segment length (host value; sizes the launch).
+ * The library reads cu_seqlens on the device only, never synchronizing with the host.  A
+ * cu_seqlens that breaks the rules above makes the call a device-side no-op (o is left
+ * unwritten); with the environment variable TS_ATTN_VALIDATE=1 the call instead synchronizes
+ * on stream and returns TS_ERR_SEGMENTS.
+ * Work scheduling: a small planning kernel orders the segments longest first and the
+ * attention kernel walks that order, so uneven batches finish with a short tail.  The plan
+ * lives in a stream-ordered device allocation made and released by the call itself
+ * (TS_ERR_NOMEM if it cannot be made).
+ */
+int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
+                       const int32_t* cu_seqlens, int32_t nseq, int32_t max_seqlen,
+                       int32_t total_tokens, int32_t H, int32_t d, float scale, void* stream);
+
+/* Human-readable name of a ts_status value (a static string; never NULL). */
+const char* ts_attn_status_str(int status);
+
+/* TS_ATTN_ABI_VERSION of the built library. */
+int ts_attn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TS_ATTN_H */

@@ -1,0 +1,11 @@
+"""MI355X (gfx950) fused segment-local attention for packed video-diffusion serving batches.
+
+The compute lives in libts_attn.so (hand-written HIP kernels behind the C ABI of
+include/ts_attn.h); this package only marshals torch tensors into that ABI.
+"""
+from .attention import ts_attn_fwd, ts_attn_fwd_varlen, default_scale  # noqa: F401
+from ._lib import TsAttnError, load, status_str  # noqa: F401
+
+
+def abi_version():
+    return load().ts_attn_abi_version()

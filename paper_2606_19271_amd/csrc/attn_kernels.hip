@@ -1,0 +1,472 @@
+// attn_kernels.hip -- gfx950 (CDNA4) kernels of the fused segment-local attention.
+//
+// Computes, for every segment s of a packed batch, token t of s and head h,
+//   O[t,h,:] = softmax_j(scale * <Q[t,h,:], K[j,h,:]>) V[j,h,:],  j over segment s (non-causal),
+// the attention of the model call that serves one coalesced chunk batch (paper Sec. 3.1), with
+// sessions kept apart as their isolated state regions require (Sec. 6.1).
+//
+// Design (one work item = one (segment, head, 256-query tile); one 512-thread workgroup each):
+//  * 8 waves, each owning 32 queries.  The wave computes S^T = K Q^T on 32x32x16 bf16 MFMAs,
+//    so that a lane holds all scores of ONE query (its column): row max and row sum are
+//    in-lane, plus one cross-half exchange (v_permlane32_swap) for the max.
+//  * The exponentiated scores P^T, packed to bf16, are already the B operand of the next
+//    product O^T += V^T P^T once the keys inside each 16-key step are taken in the order the
+//    accumulator holds them (a sum over keys does not care about their order); V^T's fragments
+//    come from row-major V in LDS through the gfx950 transpose read ds_read_b64_tr_b16.
+//  * K and V tiles of 64 keys are staged through LDS, double buffered, with padded row strides
+//    that keep the MFMA operand reads free of bank conflicts; global loads are raw buffer loads
+//    whose range check returns zeros past the segment's last row.
+//  * Online softmax in the log2 domain (exp2 with scale*log2(e) folded into one FMA).  The
+//    running maximum is only raised when a new score exceeds it by more than 2^8 in the
+//    exponent; otherwise the stale maximum is kept, which is exact in real arithmetic (the
+//    final division by the running sum cancels any common factor) and only lets P grow to
+//    at most 2^8 -- so the fp32 rescale of the O accumulator is skipped on almost every tile.
+//  * Scheduling: the launch has one workgroup per item; blockIdx is remapped so that the 32
+//    workgroups resident at once on one XCD (the hardware deals workgroups to the 8 XCDs
+//    round robin) take 32 consecutive query tiles of the same head and share its K/V in that
+//    XCD's L2.  For packed batches a planning kernel first orders segments longest first.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn_launch.h"
+
+namespace tsattn {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr int kBM = 256;       // queries per work item
+constexpr int kBN = 64;        // keys per K/V tile
+constexpr int kWaves = 8;      // waves per workgroup, 32 queries each
+constexpr int kThreads = kWaves * 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max must move
+constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
+
+template <int D>
+struct Geo {
+  static constexpr int kChunks = D / 8;                     // 16-byte chunks per row
+  static constexpr int kKRow = D * 2 + 16;                  // K row stride in LDS (bytes)
+  static constexpr int kVRow = D * 2 + 64;                  // V row stride in LDS (bytes)
+  static constexpr int kKTile = kBN * kKRow;
+  static constexpr int kVTile = kBN * kVRow;
+  static constexpr int kLoads = kBN * kChunks / kThreads;   // 16-byte loads per thread per tile
+  static constexpr int kLds = 2 * (kKTile + kVTile);        // double buffered
+  static_assert(kLoads >= 1 && kBN * kChunks % kThreads == 0, "tile must split evenly");
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// max over the two 32-lane halves of the wave (lane l and lane l^32).
+__device__ __forceinline__ float half_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// One work item: queries [q_begin, q_begin + kBM) of a segment, head h.
+struct Item {
+  int64_t seg_start;  // first token of the segment
+  int seg_len;        // tokens in the segment
+  int h;              // head
+  int q_begin;        // first query of the tile, relative to the segment
+};
+
+// XCD-aware order: workgroup b runs on XCD b % 8; consecutive workgroups of one XCD take
+// `chunk` consecutive items, and every 8*chunk workgroups cover 8*chunk consecutive items,
+// so the global order is kept at that granularity.  Bijective on [0, total).
+__device__ __forceinline__ int remap_block(int b, int total, int chunk) {
+  int span = 8 * chunk;
+  int full = (total / span) * span;
+  if (b >= full) return b;
+  int x = b & 7, j = b >> 3;
+  return (j / chunk) * span + x * chunk + (j % chunk);
+}
+
+template <int D, bool kMasked>
+__device__ __forceinline__ void attend_tile(const char* __restrict__ kt, const char* __restrict__ vt,
+                                            const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
+                                            float& m_c, float& l_part, float c, int keys_valid,
+                                            int lane) {
+  using G = Geo<D>;
+  const int hb = lane >> 5;  // which half of the wave
+  const int col = lane & 31;
+  // ---- S^T = K Q^T : two 32-key blocks, each an accumulation over d in steps of 16
+  f32x16 s[kBN / 32];
+#pragma unroll
+  for (int kb = 0; kb < kBN / 32; ++kb) {
+    s[kb] = f32x16{};
+    const char* krow = kt + (32 * kb + col) * G::kKRow + hb * 16;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
+      s[kb] = mfma32(a, qf[kk], s[kb]);
+    }
+  }
+  // accumulator register r of block kb holds key 32*kb + 8*(r/4) + 4*hb + r%4 of this tile
+  if (kMasked) {
+#pragma unroll
+    for (int kb = 0; kb < kBN / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int key = 32 * kb + 8 * (r >> 2) + 4 * hb + (r & 3);
+        if (key >= keys_valid) s[kb][r] = -INFINITY;
+      }
+  }
+  // ---- row max (the lane's query) over the tile
+  float mt = s[0][0];
+#pragma unroll
+  for (int kb = 0; kb < kBN / 32; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+  mt = half_max(mt);
+  float mt_c = mt * c;  // c >= 0, so the max commutes with the scaling
+  // ---- lazy rescale: move the running max only when P could exceed 2^kLazyRescale
+  if (__builtin_amdgcn_ballot_w64(mt_c > m_c + kLazyRescale) != 0) {
+    float m_new = fmaxf(m_c, mt_c);
+    float alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
+    l_part *= alpha;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    m_c = m_new;
+  }
+  // ---- P = exp2(S*c - m_c), bf16, row sums, and O^T += V^T P^T
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const int g = lane >> 4, i16 = lane & 15;
+  const int vr = 4 * (g >> 1) + (i16 >> 2);            // row inside an 8-key group
+  const int vc = 32 * (g & 1) + 8 * (i16 & 3);         // byte column inside a 64-byte block
+  const char* vbase = vt + vr * G::kVRow + vc;
+#pragma unroll
+  for (int t = 0; t < kBN / 16; ++t) {
+    bf16x8 p;
+#pragma unroll
+    for (int m = 0; m < 8; m += 2) {
+      float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
+      float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x0, c, -m_c));
+      float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x1, c, -m_c));
+      if (kMasked) {
+        int key0 = 16 * t + 8 * (m >> 2) + 4 * hb + (m & 3);
+        if (key0 >= keys_valid) e0 = 0.0f;
+        if (key0 + 1 >= keys_valid) e1 = 0.0f;
+      }
+      f32x2 e = {e0, e1};
+      bf16x2 pb = __builtin_convertvector(e, bf16x2);
+      p[m] = pb[0];
+      p[m + 1] = pb[1];
+      l_part = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_part, false);
+    }
+    // V^T fragment: keys 16t + {4hb + 0..3} then 16t + 8 + {4hb + 0..3}, channels 32db + col
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const char* va = vbase + (16 * t) * G::kVRow + db * 64;
+      bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va));
+      bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * G::kVRow));
+      bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+      o[db] = mfma32(a, p, o[db]);
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void load_tile(__amdgpu_buffer_rsrc_t rs, int key0, int row_bytes,
+                                          int tid, u32x4 (&r)[Geo<D>::kLoads]) {
+  using G = Geo<D>;
+#pragma unroll
+  for (int u = 0; u < G::kLoads; ++u) {
+    int cidx = tid + kThreads * u;
+    int row = cidx / G::kChunks, ch = cidx % G::kChunks;
+    r[u] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + row) * row_bytes + ch * 16, 0, 0);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_tile(char* lds, int row_stride, int tid,
+                                           const u32x4 (&r)[Geo<D>::kLoads]) {
+  using G = Geo<D>;
+#pragma unroll
+  for (int u = 0; u < G::kLoads; ++u) {
+    int cidx = tid + kThreads * u;
+    int row = cidx / G::kChunks, ch = cidx % G::kChunks;
+    *reinterpret_cast<u32x4*>(lds + row * row_stride + ch * 16) = r[u];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
+                                         const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+                                         __bf16* __restrict__ o, int H, float c, bool negate_q,
+                                         char* smem) {
+  using G = Geo<D>;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hb = lane >> 5, col = lane & 31;
+  const int row_bytes = H * D * 2;
+  const int64_t base = (it.seg_start * H + it.h) * D;  // element offset of (first token, h)
+  const uint32_t seg_bytes = (uint32_t)(it.seg_len - 1) * (uint32_t)row_bytes + D * 2;
+  __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, seg_bytes);
+  __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, seg_bytes);
+  __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, seg_bytes);
+  __amdgpu_buffer_rsrc_t ro = make_rsrc(o + base, seg_bytes);
+
+  // Q fragments (B operand of S^T = K Q^T): query col of this wave, channels 16kk + 8hb + 0..7
+  const int qrow = it.q_begin + 32 * wave + col;
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) {
+    u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(rq, qrow * row_bytes + (2 * kk + hb) * 16, 0, 0);
+    if (negate_q) raw ^= u32x4{0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u};
+    qf[kk] = __builtin_bit_cast(bf16x8, raw);
+  }
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
+  float m_c = -INFINITY, l_part = 0.0f;
+
+  char* kbuf[2] = {smem, smem + G::kKTile};
+  char* vbuf[2] = {smem + 2 * G::kKTile, smem + 2 * G::kKTile + G::kVTile};
+  const int ntiles = (it.seg_len + kBN - 1) / kBN;
+  const int nfull = it.seg_len / kBN;
+
+  u32x4 kr[G::kLoads], vr[G::kLoads];
+  load_tile<D>(rk, 0, row_bytes, tid, kr);
+  load_tile<D>(rv, 0, row_bytes, tid, vr);
+  store_tile<D>(kbuf[0], G::kKRow, tid, kr);
+  store_tile<D>(vbuf[0], G::kVRow, tid, vr);
+  __syncthreads();
+
+  for (int j = 0; j < ntiles; ++j) {
+    const int cur = j & 1;
+    const bool more = j + 1 < ntiles;
+    if (more) {
+      load_tile<D>(rk, (j + 1) * kBN, row_bytes, tid, kr);
+      load_tile<D>(rv, (j + 1) * kBN, row_bytes, tid, vr);
+    }
+    if (j < nfull)
+      attend_tile<D, false>(kbuf[cur], vbuf[cur], qf, oacc, m_c, l_part, c, kBN, lane);
+    else
+      attend_tile<D, true>(kbuf[cur], vbuf[cur], qf, oacc, m_c, l_part, c, it.seg_len - j * kBN,
+                           lane);
+    if (more) {
+      store_tile<D>(kbuf[cur ^ 1], G::kKRow, tid, kr);
+      store_tile<D>(vbuf[cur ^ 1], G::kVRow, tid, vr);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: O = O / l, bf16, rows past the segment end are dropped by the range check
+  const float l_tot = half_sum(l_part);
+  const float inv = 1.0f / l_tot;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      f32x4 x = {oacc[db][4 * g4] * inv, oacc[db][4 * g4 + 1] * inv, oacc[db][4 * g4 + 2] * inv,
+                 oacc[db][4 * g4 + 3] * inv};
+      bf16x4 b = __builtin_convertvector(x, bf16x4);
+      u32x2 w = __builtin_bit_cast(u32x2, b);
+      const int ch = 32 * db + 8 * g4 + 4 * hb;  // first of 4 channels
+      __builtin_amdgcn_raw_buffer_store_b64(w, ro, qrow * row_bytes + ch * 2, 0, 0);
+    }
+}
+
+template <int D>
+__global__ void __launch_bounds__(kThreads)
+attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
+                  const __bf16* __restrict__ v, __bf16* __restrict__ o, int L, int H, int nq,
+                  int total, int chunk, float c, int negate_q) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int item = remap_block(blockIdx.x, total, chunk);
+  const int bh = item / nq;
+  Item it;
+  it.seg_len = L;
+  it.seg_start = (int64_t)(bh / H) * L;
+  it.h = bh % H;
+  it.q_begin = (item % nq) * kBM;
+  run_item<D>(it, q, k, v, o, H, c, negate_q != 0, smem);
+}
+
+// plan layout (int32): [0] item count, [1] error flag, then per rank r (longest segment
+// first): [2 + 2r] segment index, [3 + 2r] first item of that segment.
+template <int D>
+__global__ void __launch_bounds__(kThreads)
+attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
+                   const __bf16* __restrict__ v, __bf16* __restrict__ o,
+                   const int32_t* __restrict__ cu, const int32_t* __restrict__ plan, int nseq,
+                   int H, int chunk, float c, int negate_q) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int total = plan[0];
+  if ((int)blockIdx.x >= total) return;
+  const int item = remap_block(blockIdx.x, total, chunk);
+  // last rank whose first item is <= item (empty segments share starts with the next rank)
+  int lo = 0, hi = nseq;  // plan[3 + 2*lo] <= item < plan[3 + 2*hi] (with hi = nseq as +inf)
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (plan[3 + 2 * mid] <= item) lo = mid; else hi = mid;
+  }
+  const int s = plan[2 + 2 * lo];
+  const int local = item - plan[3 + 2 * lo];
+  Item it;
+  it.seg_start = cu[s];
+  it.seg_len = cu[s + 1] - cu[s];
+  const int nq = (it.seg_len + kBM - 1) / kBM;
+  it.h = local / nq;
+  it.q_begin = (local % nq) * kBM;
+  run_item<D>(it, q, k, v, o, H, c, negate_q != 0, smem);
+}
+
+// ---- planning kernel: validate cu_seqlens, order segments longest first, prefix-sum items.
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanSortMax = 4096;  // larger batches keep their given order
+
+__global__ void __launch_bounds__(kPlanThreads)
+plan_kernel(const int32_t* __restrict__ cu, int nseq, int max_seqlen, int total_tokens, int H,
+            int32_t* __restrict__ plan) {
+  __shared__ uint64_t keys[kPlanSortMax];
+  __shared__ int32_t scan[kPlanThreads];
+  const int tid = threadIdx.x;
+  int bad = 0;
+  if (tid == 0 && (cu[0] != 0 || cu[nseq] != total_tokens)) bad = 1;
+  for (int s = tid; s < nseq; s += kPlanThreads) {
+    int len = cu[s + 1] - cu[s];
+    if (len < 0 || len > max_seqlen) bad = 1;
+  }
+  if (__syncthreads_or(bad)) {
+    if (tid == 0) { plan[0] = 0; plan[1] = 1; }
+    return;
+  }
+  const bool sorted = nseq <= kPlanSortMax;
+  if (sorted) {
+    int n2 = 1;
+    while (n2 < nseq) n2 <<= 1;
+    // key: (max - length) in the high word, index in the low word -> ascending = longest first
+    for (int i = tid; i < n2; i += kPlanThreads) {
+      if (i < nseq) {
+        uint32_t len = (uint32_t)(cu[i + 1] - cu[i]);
+        keys[i] = ((uint64_t)(0x7fffffffu - len) << 32) | (uint32_t)i;
+      } else {
+        keys[i] = ~0ull;
+      }
+    }
+    __syncthreads();
+    for (int size = 2; size <= n2; size <<= 1)
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int i = tid; i < n2; i += kPlanThreads) {
+          int jx = i ^ stride;
+          if (jx > i) {
+            bool up = (i & size) == 0;
+            uint64_t a = keys[i], b = keys[jx];
+            if ((a > b) == up) { keys[i] = b; keys[jx] = a; }
+          }
+        }
+        __syncthreads();
+      }
+  }
+  // exclusive prefix sum of H * ceil(len / kBM) in rank order, 1024 ranks per pass
+  int carry = 0;
+  for (int base = 0; base < nseq; base += kPlanThreads) {
+    int r = base + tid;
+    int seg = 0, cnt = 0;
+    if (r < nseq) {
+      seg = sorted ? (int)(keys[r] & 0xffffffffu) : r;
+      int len = cu[seg + 1] - cu[seg];
+      cnt = H * ((len + kBM - 1) / kBM);
+    }
+    scan[tid] = cnt;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {
+      int add = tid >= off ? scan[tid - off] : 0;
+      __syncthreads();
+      scan[tid] += add;
+      __syncthreads();
+    }
+    if (r < nseq) {
+      plan[2 + 2 * r] = seg;
+      plan[3 + 2 * r] = carry + scan[tid] - cnt;
+    }
+    carry += scan[kPlanThreads - 1];
+    __syncthreads();
+  }
+  if (tid == 0) { plan[0] = carry; plan[1] = 0; }
+}
+
+// ---------------------------------------------------------------------------------------------
+// host-side launchers
+
+template <int D>
+static hipError_t launch_dense_d(const DenseArgs& a, hipStream_t st) {
+  const int nq = (a.L + kBM - 1) / kBM;
+  const int total = a.B * a.H * nq;
+  const float c = fabsf(a.scale) * kLog2e;
+  hipLaunchKernelGGL((attn_dense_kernel<D>), dim3(total), dim3(kThreads), Geo<D>::kLds, st,
+                     (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
+                     a.L, a.H, nq, total, a.xcd_chunk, c, a.scale < 0.0f ? 1 : 0);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_varlen_d(const VarlenArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a.cu_seqlens, a.nseq,
+                     a.max_seqlen, a.total_tokens, a.H, a.plan);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t grid = varlen_grid_bound(a.total_tokens, a.nseq, a.H);
+  const float c = fabsf(a.scale) * kLog2e;
+  hipLaunchKernelGGL((attn_varlen_kernel<D>), dim3((unsigned)grid), dim3(kThreads), Geo<D>::kLds,
+                     st, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
+                     (__bf16*)a.o, a.cu_seqlens, a.plan, a.nseq, a.H, a.xcd_chunk, c,
+                     a.scale < 0.0f ? 1 : 0);
+  return hipGetLastError();
+}
+
+int64_t varlen_grid_bound(int32_t total_tokens, int32_t nseq, int32_t H) {
+  // sum_s ceil(L_s / BM) <= ceil(T / BM) + nseq
+  return (int64_t)H * (((int64_t)total_tokens + kBM - 1) / kBM + nseq);
+}
+
+int64_t plan_ints(int32_t nseq) { return 2 + 2 * (int64_t)nseq; }
+
+int query_tile() { return kBM; }
+
+hipError_t configure_kernels() {
+  hipError_t e;
+  e = hipFuncSetAttribute((const void*)attn_dense_kernel<64>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<64>::kLds);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)attn_dense_kernel<128>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<128>::kLds);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)attn_varlen_kernel<64>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<64>::kLds);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void*)attn_varlen_kernel<128>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, Geo<128>::kLds);
+}
+
+hipError_t launch_dense(const DenseArgs& a, hipStream_t st) {
+  return a.d == 64 ? launch_dense_d<64>(a, st) : launch_dense_d<128>(a, st);
+}
+
+hipError_t launch_varlen(const VarlenArgs& a, hipStream_t st) {
+  return a.d == 64 ? launch_varlen_d<64>(a, st) : launch_varlen_d<128>(a, st);
+}
+
+}  // namespace tsattn

@@ -1,0 +1,121 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol, and rejects bad
+arguments on the host before any HIP call (fake pointers are never dereferenced)."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ts_attn.h")
+
+ts = pytest.importorskip("paper_2606_19271_amd")
+from paper_2606_19271_amd import _lib  # noqa: E402
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ts_attn_\w+)\s*\(", text)))
+
+
+def header_macro(name):
+    m = re.search(r"#define\s+%s\s+(\d+)" % name, open(HEADER).read())
+    return int(m.group(1))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert names == ["ts_attn_abi_version", "ts_attn_fwd", "ts_attn_fwd_varlen",
+                     "ts_attn_status_str"]
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (ts_attn_\w+)", out))
+    assert set(names) <= exported
+
+
+def test_abi_version_matches_header(lib):
+    assert lib.ts_attn_abi_version() == header_macro("TS_ATTN_ABI_VERSION")
+
+
+def test_header_compiles_as_c_and_cxx(tmp_path):
+    src = tmp_path / "use.c"
+    src.write_text('#include "ts_attn.h"\nint main(void){return ts_attn_abi_version() - TS_ATTN_ABI_VERSION;}\n')
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-I", os.path.dirname(HEADER),
+                    str(src)], check=True)
+    subprocess.run(["g++", "-std=c++11", "-Wall", "-Werror", "-fsyntax-only", "-x", "c++",
+                    "-I", os.path.dirname(HEADER), str(src)], check=True)
+
+
+def test_status_strings(lib):
+    for code, name in enumerate(_lib.STATUS_NAMES):
+        assert ts.status_str(code).startswith(name)
+    assert ts.status_str(999) == "unknown ts_status"
+
+
+A = 0x10000          # fake, 16-byte aligned device addresses; never dereferenced
+BIG = 0x100000000000  # far from A: no overlap for the sizes below
+
+
+def fwd(lib, q=A, k=A, v=A, o=BIG, B=1, L=128, H=2, d=128, scale=0.125, stream=None):
+    P = ctypes.c_void_p
+    return lib.ts_attn_fwd(P(q), P(k), P(v), P(o), B, L, H, d, scale, P(stream))
+
+
+def varlen(lib, q=A, k=A, v=A, o=BIG, cu=A, nseq=2, max_seqlen=64, T=128, H=2, d=128,
+           scale=0.125):
+    P = ctypes.c_void_p
+    return lib.ts_attn_fwd_varlen(P(q), P(k), P(v), P(o), P(cu), nseq, max_seqlen, T, H, d, scale,
+                                  P(None))
+
+
+def test_dense_argument_checks(lib):
+    assert fwd(lib, q=0) == _lib.TS_ERR_NULL
+    assert fwd(lib, o=0) == _lib.TS_ERR_NULL
+    assert fwd(lib, B=-1) == _lib.TS_ERR_SHAPE
+    assert fwd(lib, L=-5) == _lib.TS_ERR_SHAPE
+    assert fwd(lib, H=0) == _lib.TS_ERR_SHAPE
+    for d in (0, 32, 96, 256):
+        assert fwd(lib, d=d) == _lib.TS_ERR_HEAD_DIM
+    for s in (math.nan, math.inf, -math.inf):
+        assert fwd(lib, scale=s) == _lib.TS_ERR_SCALE
+    assert fwd(lib, k=A + 8) == _lib.TS_ERR_ALIGN
+    assert fwd(lib, o=BIG + 2) == _lib.TS_ERR_ALIGN
+    assert fwd(lib, o=A) == _lib.TS_ERR_ALIAS                      # o == q
+    assert fwd(lib, v=BIG + 4096, o=BIG) == _lib.TS_ERR_ALIAS      # o overlaps v
+    assert fwd(lib, L=300000, H=40) == _lib.TS_ERR_SHAPE           # beyond the byte limit
+    # empty problems are no-ops that never touch the device
+    assert fwd(lib, B=0) == _lib.TS_OK
+    assert fwd(lib, L=0) == _lib.TS_OK
+
+
+def test_varlen_argument_checks(lib):
+    assert varlen(lib, cu=0) == _lib.TS_ERR_NULL
+    assert varlen(lib, nseq=-1) == _lib.TS_ERR_SHAPE
+    assert varlen(lib, max_seqlen=-1) == _lib.TS_ERR_SHAPE
+    assert varlen(lib, T=-1) == _lib.TS_ERR_SHAPE
+    assert varlen(lib, d=80) == _lib.TS_ERR_HEAD_DIM
+    assert varlen(lib, scale=math.nan) == _lib.TS_ERR_SCALE
+    assert varlen(lib, q=A + 1) == _lib.TS_ERR_ALIGN
+    assert varlen(lib, o=A) == _lib.TS_ERR_ALIAS
+    assert varlen(lib, nseq=1 << 24, T=1 << 24) == _lib.TS_ERR_SHAPE  # grid too large
+    assert varlen(lib, nseq=0) == _lib.TS_OK
+    assert varlen(lib, T=0) == _lib.TS_OK
+
+
+def test_python_binding_rejects_cpu_tensors():
+    import torch
+    x = torch.zeros((1, 8, 1, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        ts.ts_attn_fwd(x, x, x)
+    with pytest.raises(ValueError):
+        ts.ts_attn_fwd_varlen(x[0], x[0], x[0], torch.tensor([0, 8], dtype=torch.int32), 8)
