@@ -1,0 +1,194 @@
+"""Benchmark of the fused segment-local attention on one MI355X.
+
+One step = one call of the fused attention over a whole workload (by default the 32760-token,
+40-head, d=128 latent of a large video DiT: 21 frames x 30 x 52), inputs already resident in HBM.
+Prints one JSON line:
+  value         attention TFLOP/s = sum_s 4 L_s^2 d H / (wall time per step)
+  roofline      the kernel's algorithmic flops / its average launch time (HIP events on the
+                launch stream) against the dense bf16 MFMA peak of MI355X; traffic = HBM bytes per
+                launch from a committed rocprofv3 FETCH_SIZE/WRITE_SIZE measurement of the same
+                kernel source (null when the kernel source changed since)
+  cpu_baseline  the fp64 oracle timed on this host's cores on a bounded row sample of the same
+                workload, in the same unit; the sampled rows also serve as a parity check
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--cpu-seconds S]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_19271_amd", "csrc", "attn_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+METRIC = "attention TFLOPS (4·L²·d·H) + % bf16 MFMA peak at L=32760,H=40,d=128"
+
+
+def kernel_sha():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_bytes(workload):
+    """HBM bytes per launch measured by rocprofv3 for this exact kernel source, else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = t.get(workload)
+    if not e or e.get("kernel_sha") != kernel_sha():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(w, q, k, v, o_gpu, seconds):
+    """Times the oracle on batches of sampled rows until `seconds` of CPU time have elapsed."""
+    import numpy as np
+
+    import workloads as W
+    from oracle import ts_ref
+
+    ts_ref.load()
+    row_t, row_h = W.sample_rows(w, n_random=4096, seed=999)
+    perm = np.random.default_rng(7).permutation(row_t.size)
+    row_t, row_h = row_t[perm], row_h[perm]
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    cu = w.cu_seqlens
+    seg_len = np.diff(cu)
+    seg_of = np.searchsorted(cu, row_t, side="right") - 1
+    done, flops, t_total, batch = 0, 0.0, 0.0, 64
+    refs = []
+    while t_total < seconds and done < row_t.size:
+        sl = slice(done, min(done + batch, row_t.size))
+        t0 = time.perf_counter()
+        refs.append(ts_ref.attn_rows(qb, kb, vb, cu, w.scale, row_t[sl], row_h[sl]))
+        t_total += time.perf_counter() - t0
+        flops += float(np.sum(4.0 * seg_len[seg_of[sl]] * w.d))
+        done = sl.stop
+        batch = min(batch * 2, 1024)
+    ref = np.concatenate(refs)
+    got = o_gpu[row_t[:done], row_h[:done]].astype(np.float64)
+    err = np.abs(got - ref)
+    return {
+        "value": flops / t_total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": ts_ref.num_threads(),
+        "kind": "oracle",
+        "sample": "%d (token, head) rows of %s (%.3g fp64 GFLOP of the %.3g GFLOP call), %.1f s"
+                  % (done, w.name, flops / 1e9, w.flops / 1e9, t_total),
+    }, {"rows": int(done), "max_abs": float(err.max()), "mean_abs": float(err.mean())}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dit_large")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="instead of attention, time a plain device copy of this many bytes "
+                         "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known traffic)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the attention of a packed batch runs on the GPU "
+              "that holds its sessions, with no exchange between GPUs; run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_19271_amd as ts
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.copy_bytes:
+        src = torch.ones(args.copy_bytes // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        print(json.dumps({"copy_bytes": src.numel() * 2, "ms": dt * 1e3,
+                          "GB/s_read_plus_write": 2 * src.numel() * 2 / dt / 1e9}), flush=True)
+        return
+
+    w = W.WORKLOADS[args.workload]
+    q, k, v = W.make_inputs(w)
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    cu = torch.tensor(w.cu_seqlens, device=dev)
+    dense = len(w.seqlens) == 1
+    out = torch.empty_like(qd)
+
+    def step():
+        if dense:
+            ts.ts_attn_fwd(qd.view(1, w.T, w.H, w.d), kd.view(1, w.T, w.H, w.d),
+                           vd.view(1, w.T, w.H, w.d), out=out.view(1, w.T, w.H, w.d))
+        else:
+            ts.ts_attn_fwd_varlen(qd, kd, vd, cu, w.max_seqlen, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    ms_per_step = wall / args.steps * 1e3
+    value = w.flops / (ms_per_step * 1e-3) / 1e12
+    kernel_ms = float(np.mean(launch_ms))
+    achieved = w.flops / (kernel_ms * 1e-3) / 1e12
+    traffic = traffic_bytes(w.name)
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "segments": list(w.seqlens), "T": w.T, "H": w.H, "d": w.d,
+                   "causal": False, "flops_per_call": w.flops, "hbm_bytes_per_call": w.hbm_bytes,
+                   "kernel_ms_mean": kernel_ms, "kernel_ms_min": float(np.min(launch_ms)),
+                   "kernel_ms_max": float(np.max(launch_ms)),
+                   "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        o_host = out.float().cpu().numpy()
+        del qd, kd, vd
+        base, parity = cpu_baseline(w, q, k, v, o_host, args.cpu_seconds)
+        result["cpu_baseline"] = base
+        result["parity_sample"] = parity
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -41,6 +41,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr int kBM = 256;       // queries per work item
 constexpr int kBN = 64;        // keys per K/V tile
@@ -101,7 +104,7 @@ __device__ __forceinline__ int remap_block(int b, int total, int chunk) {
 }
 
 template <int D, bool kMasked>
-__device__ __forceinline__ void attend_tile(const char* __restrict__ kt, const char* __restrict__ vt,
+__device__ __forceinline__ void attend_tile(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
                                             const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
                                             float& m_c, float& l_part, float c, int keys_valid,
                                             int lane) {
@@ -113,10 +116,10 @@ __device__ __forceinline__ void attend_tile(const char* __restrict__ kt, const c
 #pragma unroll
   for (int kb = 0; kb < kBN / 32; ++kb) {
     s[kb] = f32x16{};
-    const char* krow = kt + (32 * kb + col) * G::kKRow + hb * 16;
+    const lds_char* krow = kt + (32 * kb + col) * G::kKRow + hb * 16;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
-      bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
+      bf16x8 a = *(const lds_bf16x8*)(krow + kk * 32);
       s[kb] = mfma32(a, qf[kk], s[kb]);
     }
   }
@@ -151,13 +154,15 @@ __device__ __forceinline__ void attend_tile(const char* __restrict__ kt, const c
   }
   // ---- P = exp2(S*c - m_c), bf16, row sums, and O^T += V^T P^T
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float lsum[kBN / 16];  // independent partial row sums, one per 16-key step
   const int g = lane >> 4, i16 = lane & 15;
   const int vr = 4 * (g >> 1) + (i16 >> 2);            // row inside an 8-key group
   const int vc = 32 * (g & 1) + 8 * (i16 & 3);         // byte column inside a 64-byte block
-  const char* vbase = vt + vr * G::kVRow + vc;
+  const lds_char* vbase = vt + vr * G::kVRow + vc;
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t) {
     bf16x8 p;
+    lsum[t] = 0.0f;
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
       float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
@@ -172,18 +177,22 @@ __device__ __forceinline__ void attend_tile(const char* __restrict__ kt, const c
       bf16x2 pb = __builtin_convertvector(e, bf16x2);
       p[m] = pb[0];
       p[m + 1] = pb[1];
-      l_part = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, l_part, false);
+      lsum[t] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum[t], false);
     }
     // V^T fragment: keys 16t + {4hb + 0..3} then 16t + 8 + {4hb + 0..3}, channels 32db + col
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const char* va = vbase + (16 * t) * G::kVRow + db * 64;
+      const lds_char* va = vbase + (16 * t) * G::kVRow + db * 64;
       bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va));
       bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * G::kVRow));
       bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
       o[db] = mfma32(a, p, o[db]);
     }
   }
+  float lt = lsum[0];
+#pragma unroll
+  for (int t = 1; t < kBN / 16; ++t) lt += lsum[t];
+  l_part += lt;
 }
 
 template <int D>
@@ -199,14 +208,14 @@ __device__ __forceinline__ void load_tile(__amdgpu_buffer_rsrc_t rs, int key0, i
 }
 
 template <int D>
-__device__ __forceinline__ void store_tile(char* lds, int row_stride, int tid,
+__device__ __forceinline__ void store_tile(lds_char* lds, int row_stride, int tid,
                                            const u32x4 (&r)[Geo<D>::kLoads]) {
   using G = Geo<D>;
 #pragma unroll
   for (int u = 0; u < G::kLoads; ++u) {
     int cidx = tid + kThreads * u;
     int row = cidx / G::kChunks, ch = cidx % G::kChunks;
-    *reinterpret_cast<u32x4*>(lds + row * row_stride + ch * 16) = r[u];
+    *(lds_u32x4*)(lds + row * row_stride + ch * 16) = r[u];
   }
 }
 
@@ -241,35 +250,38 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
   for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
   float m_c = -INFINITY, l_part = 0.0f;
 
-  char* kbuf[2] = {smem, smem + G::kKTile};
-  char* vbuf[2] = {smem + 2 * G::kKTile, smem + 2 * G::kKTile + G::kVTile};
+  lds_char* const lds = (lds_char*)smem;
   const int ntiles = (it.seg_len + kBN - 1) / kBN;
   const int nfull = it.seg_len / kBN;
 
   u32x4 kr[G::kLoads], vr[G::kLoads];
   load_tile<D>(rk, 0, row_bytes, tid, kr);
   load_tile<D>(rv, 0, row_bytes, tid, vr);
-  store_tile<D>(kbuf[0], G::kKRow, tid, kr);
-  store_tile<D>(vbuf[0], G::kVRow, tid, vr);
+  store_tile<D>(lds, G::kKRow, tid, kr);
+  store_tile<D>(lds + 2 * G::kKTile, G::kVRow, tid, vr);
   __syncthreads();
 
-  for (int j = 0; j < ntiles; ++j) {
+  // full tiles: no masking; the next tile's loads are in flight while this one is computed
+  for (int j = 0; j < nfull; ++j) {
     const int cur = j & 1;
     const bool more = j + 1 < ntiles;
     if (more) {
       load_tile<D>(rk, (j + 1) * kBN, row_bytes, tid, kr);
       load_tile<D>(rv, (j + 1) * kBN, row_bytes, tid, vr);
     }
-    if (j < nfull)
-      attend_tile<D, false>(kbuf[cur], vbuf[cur], qf, oacc, m_c, l_part, c, kBN, lane);
-    else
-      attend_tile<D, true>(kbuf[cur], vbuf[cur], qf, oacc, m_c, l_part, c, it.seg_len - j * kBN,
-                           lane);
+    attend_tile<D, false>(lds + cur * G::kKTile, lds + 2 * G::kKTile + cur * G::kVTile, qf, oacc,
+                          m_c, l_part, c, kBN, lane);
     if (more) {
-      store_tile<D>(kbuf[cur ^ 1], G::kKRow, tid, kr);
-      store_tile<D>(vbuf[cur ^ 1], G::kVRow, tid, vr);
+      store_tile<D>(lds + (cur ^ 1) * G::kKTile, G::kKRow, tid, kr);
+      store_tile<D>(lds + 2 * G::kKTile + (cur ^ 1) * G::kVTile, G::kVRow, tid, vr);
     }
     __syncthreads();
+  }
+  // the ragged last tile, keys past the segment end masked
+  if (nfull < ntiles) {
+    const int cur = nfull & 1;
+    attend_tile<D, true>(lds + cur * G::kKTile, lds + 2 * G::kKTile + cur * G::kVTile, qf, oacc,
+                         m_c, l_part, c, it.seg_len - nfull * kBN, lane);
   }
 
   // ---- epilogue: O = O / l, bf16, rows past the segment end are dropped by the range check
