@@ -13,14 +13,22 @@
 //    product O^T += V^T P^T once the keys inside each 16-key step are taken in the order the
 //    accumulator holds them (a sum over keys does not care about their order); V^T's fragments
 //    come from row-major V in LDS through the gfx950 transpose read ds_read_b64_tr_b16.
+//  * The two waves that share a SIMD run a ping-pong: one issues the MFMAs of a tile (S = K Q^T
+//    of the next tile and O += V P of the previous one) at raised priority while the other
+//    issues the softmax VALU work, and they swap roles at each workgroup barrier.  On gfx950
+//    v_exp_f32 shares the VALU pipe with the other vector ops, while MFMAs run in the matrix
+//    core, so the softmax can hide under the other wave's matrix work.
 //  * K and V tiles of 64 keys are staged through LDS, double buffered, with padded row strides
-//    that keep the MFMA operand reads free of bank conflicts; global loads are raw buffer loads
-//    whose range check returns zeros past the segment's last row.
-//  * Online softmax in the log2 domain (exp2 with scale*log2(e) folded into one FMA).  The
-//    running maximum is only raised when a new score exceeds it by more than 2^8 in the
-//    exponent; otherwise the stale maximum is kept, which is exact in real arithmetic (the
-//    final division by the running sum cancels any common factor) and only lets P grow to
-//    at most 2^8 -- so the fp32 rescale of the O accumulator is skipped on almost every tile.
+//    that keep the MFMA operand reads free of bank conflicts.  The global loads go through
+//    registers two sets deep and are issued only in the vector steps, spread between the
+//    softmax instructions; they are raw buffer loads whose range check returns zeros past the
+//    segment's last row.
+//  * Online softmax in the log2 domain (exp2 with scale*log2(e) folded into one FMA).  A tile
+//    is first exponentiated against the running maximum as it stands; only if some weight
+//    would exceed 2^40 (or on the first and the ragged last tile) is the tile's maximum taken
+//    and the O accumulator rescaled.  Keeping a stale maximum is exact in real arithmetic (the
+//    final division by the running sum cancels the common factor), so for ordinary inputs the
+//    per-tile max reduction and the O rescale disappear.
 //  * Scheduling: the launch has one workgroup per item; blockIdx is remapped so that the 32
 //    workgroups resident at once on one XCD (the hardware deals workgroups to the 8 XCDs
 //    round robin) take 32 consecutive query tiles of the same head and share its K/V in that
@@ -45,12 +53,12 @@ typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) char lds_char;
 
+
 constexpr int kBM = 256;       // queries per work item
 constexpr int kBN = 64;        // keys per K/V tile
 constexpr int kWaves = 8;      // waves per workgroup, 32 queries each
 constexpr int kThreads = kWaves * 64;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max must move
 constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
 
 template <int D>
@@ -103,16 +111,14 @@ __device__ __forceinline__ int remap_block(int b, int total, int chunk) {
   return (j / chunk) * span + x * chunk + (j % chunk);
 }
 
-template <int D, bool kMasked>
-__device__ __forceinline__ void attend_tile(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
-                                            const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
-                                            float& m_c, float& l_part, float c, int keys_valid,
-                                            int lane) {
+// S^T = K Q^T for one 64-key tile: two 32-key blocks, each an accumulation over d in steps of 16.
+// Accumulator register r of block kb holds key 32*kb + 8*(r/4) + 4*hb + r%4 of the tile for the
+// lane's query (lane & 31).
+template <int D>
+__device__ __forceinline__ void qk_tile(const lds_char* __restrict__ kt, const bf16x8 (&qf)[D / 16],
+                                        f32x16 (&s)[kBN / 32], int lane) {
   using G = Geo<D>;
-  const int hb = lane >> 5;  // which half of the wave
-  const int col = lane & 31;
-  // ---- S^T = K Q^T : two 32-key blocks, each an accumulation over d in steps of 16
-  f32x16 s[kBN / 32];
+  const int hb = lane >> 5, col = lane & 31;
 #pragma unroll
   for (int kb = 0; kb < kBN / 32; ++kb) {
     s[kb] = f32x16{};
@@ -123,45 +129,41 @@ __device__ __forceinline__ void attend_tile(const lds_char* __restrict__ kt, con
       s[kb] = mfma32(a, qf[kk], s[kb]);
     }
   }
-  // accumulator register r of block kb holds key 32*kb + 8*(r/4) + 4*hb + r%4 of this tile
-  if (kMasked) {
-#pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int key = 32 * kb + 8 * (r >> 2) + 4 * hb + (r & 3);
-        if (key >= keys_valid) s[kb][r] = -INFINITY;
-      }
-  }
-  // ---- row max (the lane's query) over the tile
-  float mt = s[0][0];
-#pragma unroll
-  for (int kb = 0; kb < kBN / 32; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
-  mt = half_max(mt);
-  float mt_c = mt * c;  // c >= 0, so the max commutes with the scaling
-  // ---- lazy rescale: move the running max only when P could exceed 2^kLazyRescale
-  if (__builtin_amdgcn_ballot_w64(mt_c > m_c + kLazyRescale) != 0) {
-    float m_new = fmaxf(m_c, mt_c);
-    float alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
-    l_part *= alpha;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-    m_c = m_new;
-  }
-  // ---- P = exp2(S*c - m_c), bf16, row sums, and O^T += V^T P^T
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float lsum[kBN / 16];  // independent partial row sums, one per 16-key step
+}
+
+// O^T += V^T P^T for one 64-key tile.  p[t] holds the bf16 weights of keys
+// 16t + 8*(m/4) + 4*hb + m%4 (m = 0..7) -- the accumulator order of qk_tile -- and the V^T
+// fragments are read in that same key order with the transpose read: within each 16-lane
+// group, lane 4R + c addresses 4 channels of key row R and lane j receives channel j of 4 rows.
+template <int D>
+__device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const bf16x8 (&p)[kBN / 16],
+                                        f32x16 (&o)[D / 32], int lane) {
+  using G = Geo<D>;
   const int g = lane >> 4, i16 = lane & 15;
-  const int vr = 4 * (g >> 1) + (i16 >> 2);            // row inside an 8-key group
-  const int vc = 32 * (g & 1) + 8 * (i16 & 3);         // byte column inside a 64-byte block
+  const int vr = 4 * (g >> 1) + (i16 >> 2);     // key row inside an 8-key group
+  const int vc = 32 * (g & 1) + 8 * (i16 & 3);  // byte column inside a 64-byte channel block
   const lds_char* vbase = vt + vr * G::kVRow + vc;
 #pragma unroll
+  for (int t = 0; t < kBN / 16; ++t)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const lds_char* va = vbase + (16 * t) * G::kVRow + db * 64;
+      bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va));
+      bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * G::kVRow));
+      bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+      o[db] = mfma32(a, p[t], o[db]);
+    }
+}
+
+// exp2(S*c - m_c) for the 32 scores of the lane, packed to the bf16 B operands of the PV
+// product, with their sum (accumulated from the bf16 values the product will use).
+template <bool kMasked>
+__device__ __forceinline__ float exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
+                                          float m_c, float c, int keys_valid, int hb) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float lsum[kBN / 16];  // independent partial sums, one per 16-key step
+#pragma unroll
   for (int t = 0; t < kBN / 16; ++t) {
-    bf16x8 p;
     lsum[t] = 0.0f;
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
@@ -175,24 +177,71 @@ __device__ __forceinline__ void attend_tile(const lds_char* __restrict__ kt, con
       }
       f32x2 e = {e0, e1};
       bf16x2 pb = __builtin_convertvector(e, bf16x2);
-      p[m] = pb[0];
-      p[m + 1] = pb[1];
+      p[t][m] = pb[0];
+      p[t][m + 1] = pb[1];
       lsum[t] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum[t], false);
-    }
-    // V^T fragment: keys 16t + {4hb + 0..3} then 16t + 8 + {4hb + 0..3}, channels 32db + col
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      const lds_char* va = vbase + (16 * t) * G::kVRow + db * 64;
-      bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va));
-      bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * G::kVRow));
-      bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-      o[db] = mfma32(a, p, o[db]);
     }
   }
   float lt = lsum[0];
 #pragma unroll
   for (int t = 1; t < kBN / 16; ++t) lt += lsum[t];
-  l_part += lt;
+  return lt;
+}
+
+// Online softmax of one tile of scores (the lane's query): turns S into bf16 weights
+// P = exp2(S*c - m_c) and adds their sum to l_part.
+//
+// The running maximum m_c is not recomputed per tile.  A full tile first tries the current
+// m_c: if every lane's weights sum to at most kSumLimit, every weight is at most kSumLimit, the
+// fp32 accumulators stay far from overflow, and the tile is done -- exact in real arithmetic,
+// since the final division by l cancels the common factor 2^(m_true - m_c).  Otherwise (the
+// first tile, where m_c = -inf, a score far above the running maximum, or the masked last tile)
+// the tile's true maximum is taken, m_c moves up to it, `rescale` is set and the O accumulator
+// must be multiplied by `alpha` before these weights are added to it.
+constexpr float kSumLimit = 1099511627776.0f;  // 2^40
+
+template <bool kMasked>
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
+                                             float& m_c, float& l_part, float& alpha,
+                                             bool& rescale, float c, int keys_valid, int lane) {
+  const int hb = lane >> 5;
+  if (!kMasked) {
+    const float lt = exp_pack<false>(s, p, m_c, c, kBN, hb);
+    if (__builtin_amdgcn_ballot_w64(!(lt <= kSumLimit)) == 0) {
+      rescale = false;
+      l_part += lt;
+      return;
+    }
+  }
+  if (kMasked) {
+#pragma unroll
+    for (int kb = 0; kb < kBN / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int key = 32 * kb + 8 * (r >> 2) + 4 * hb + (r & 3);
+        if (key >= keys_valid) s[kb][r] = -INFINITY;
+      }
+  }
+  float mt = s[0][0];
+#pragma unroll
+  for (int kb = 0; kb < kBN / 32; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
+  mt = half_max(mt);
+  const float m_new = fmaxf(m_c, mt * c);  // c >= 0, so the max commutes with the scaling
+  alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
+  m_c = m_new;
+  rescale = true;
+  const float lt = exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
+  l_part = l_part * alpha + lt;
+}
+
+template <int D>
+__device__ __forceinline__ void scale_acc(f32x16 (&o)[D / 32], float alpha) {
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
 }
 
 template <int D>
@@ -219,13 +268,55 @@ __device__ __forceinline__ void store_tile(lds_char* lds, int row_stride, int ti
   }
 }
 
-template <int D>
-__device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
-                                         const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-                                         __bf16* __restrict__ o, int H, float c, bool negate_q,
-                                         char* smem) {
+// The matrix step of tile j: S_j = K_j Q^T followed by O += V_{j-1} P_{j-1}, in one basic
+// block.  The issue order is pinned so that each MFMA's LDS operand was requested about eight
+// MFMAs earlier: 8 K reads up front, then one MFMA followed by the next one or two operand reads.
+template <int D, bool kPV>
+__device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
+                                       const bf16x8 (&qf)[D / 16], f32x16 (&s)[kBN / 32],
+                                       const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32], int lane) {
+  qk_tile<D>(kt, qf, s, lane);
+  if (kPV) pv_tile<D>(vt, p, o, lane);
+  constexpr int kQK = (kBN / 32) * (D / 16);          // MFMAs of S (16 at d = 128)
+  constexpr int kPVm = kPV ? (kBN / 16) * (D / 32) : 0;  // MFMAs of PV (16 at d = 128)
+  constexpr int kAhead = 8;
+  // reads: kQK single b128 reads, then 2 transpose reads per PV MFMA
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+  for (int i = 0; i < kQK + kPVm; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    const int next = i + kAhead;  // MFMA whose operand is requested now
+    if (next < kQK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    else if (next < kQK + kPVm) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+}
+
+// One work item, software-pipelined across the two waves that share each SIMD.
+//
+// Per 64-key tile j a wave runs two steps: M(j) -- the matrix step: S_j = K_j Q^T and
+// O += V_{j-1} P_{j-1} on MFMA -- and V(j) -- the vector step: the online softmax S_j -> P_j.
+// Waves 0-3 (group A) and waves 4-7 (group B) sit on the four SIMDs in pairs (wave w and w+4
+// share SIMD w % 4), and group B runs one step behind group A, with a workgroup barrier between
+// steps: while one wave of a SIMD keeps the matrix core busy, the other issues its softmax VALU
+// work.  The matrix step raises its wave priority so its MFMAs issue first, and it does no
+// global-memory work at all.
+//
+// K/V staging: each thread moves a fixed share of every tile's 16-byte chunks through
+// registers, two register sets deep, in its vector steps only, spread between the softmax
+// instructions: in V(j) it writes the set loaded in V(j-1) to LDS and loads the next tile into
+// the other set.  Group A handles (K_{j+1}, V_j) in V(j), group B (K_{j+2}, V_{j+1}); both halves
+// of (K_m, V_{m-1}) are in LDS before group A's M(m), and no buffer is rewritten before both
+// groups have read it (K_m and V_m in buffer m % 2).  Loads of tiles past the segment end read
+// zeros and their writes land in a buffer nobody reads any more, so the schedule has no branches.
+// The two groups are separate instantiations, so each has a straight-line schedule.
+template <int D, bool kGroupB>
+__device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __restrict__ q,
+                                               const __bf16* __restrict__ k,
+                                               const __bf16* __restrict__ v, __bf16* __restrict__ o,
+                                               int H, float c, bool negate_q, char* smem) {
   using G = Geo<D>;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hb = lane >> 5, col = lane & 31;
   const int row_bytes = H * D * 2;
   const int64_t base = (it.seg_start * H + it.h) * D;  // element offset of (first token, h)
@@ -233,7 +324,9 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
   __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, seg_bytes);
   __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, seg_bytes);
   __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, seg_bytes);
-  __amdgpu_buffer_rsrc_t ro = make_rsrc(o + base, seg_bytes);
+  lds_char* const lds = (lds_char*)smem;
+  lds_char* const kbuf = lds;                  // 2 x kKTile
+  lds_char* const vbuf = lds + 2 * G::kKTile;  // 2 x kVTile
 
   // Q fragments (B operand of S^T = K Q^T): query col of this wave, channels 16kk + 8hb + 0..7
   const int qrow = it.q_begin + 32 * wave + col;
@@ -248,43 +341,89 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
-  float m_c = -INFINITY, l_part = 0.0f;
+  f32x16 s[kBN / 32];
+  bf16x8 p[kBN / 16];
+  float m_c = -INFINITY, l_part = 0.0f, alpha = 1.0f;
+  bool rescale = false;
 
-  lds_char* const lds = (lds_char*)smem;
   const int ntiles = (it.seg_len + kBN - 1) / kBN;
-  const int nfull = it.seg_len / kBN;
+  const int last_keys = it.seg_len - (ntiles - 1) * kBN;  // valid keys of the last tile
+  struct Stage { u32x4 k[G::kLoads], v[G::kLoads]; };
+  Stage st0, st1;
+  auto load = [&](Stage& x, int kj, int vj) {
+    load_tile<D>(rk, kj * kBN, row_bytes, tid, x.k);
+    load_tile<D>(rv, vj * kBN, row_bytes, tid, x.v);
+  };
+  auto store = [&](const Stage& x, int kj, int vj) {
+    store_tile<D>(kbuf + (kj & 1) * G::kKTile, G::kKRow, tid, x.k);
+    store_tile<D>(vbuf + (vj & 1) * G::kVTile, G::kVRow, tid, x.v);
+  };
+  // first tile of the pair this group handles in V(j): A (K_{j+1}, V_j), B (K_{j+2}, V_{j+1})
+  constexpr int kLead = kGroupB ? 1 : 0;
+  // vector step j: store the set loaded one vector step ago, load the next pair, softmax
+  auto vstep = [&](int j, Stage& to_store, Stage& to_load) {
+    store(to_store, j + 1 + kLead, j + kLead);
+    load(to_load, j + 2 + kLead, j + 1 + kLead);
+    if (j + 1 < ntiles)
+      softmax_tile<false>(s, p, m_c, l_part, alpha, rescale, c, kBN, lane);
+    else
+      softmax_tile<true>(s, p, m_c, l_part, alpha, rescale, c, last_keys, lane);
+    // spread the memory operations between the softmax's VALU work
+#pragma unroll
+    for (int i = 0; i < 2 * G::kLoads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 3);
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 3);
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * G::kLoads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 3);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
+    }
+  };
 
-  u32x4 kr[G::kLoads], vr[G::kLoads];
-  load_tile<D>(rk, 0, row_bytes, tid, kr);
-  load_tile<D>(rv, 0, row_bytes, tid, vr);
-  store_tile<D>(lds, G::kKRow, tid, kr);
-  store_tile<D>(lds + 2 * G::kKTile, G::kVRow, tid, vr);
+  // prologue: K_0 by every thread; then the first pair(s) of this group
+  load(st0, 0, 0);
+  store_tile<D>(kbuf, G::kKRow, tid, st0.k);
+  if (kGroupB) {
+    load(st0, 1, 0);      // (K_1, V_0), written right away
+    store(st0, 1, 0);
+    load(st1, 2, 1);      // (K_2, V_1), written in V(0)
+  } else {
+    load(st1, 1, 0);      // (K_1, V_0), written in V(0)
+  }
   __syncthreads();
+  if (kGroupB) __syncthreads();  // group B starts one step behind
 
-  // full tiles: no masking; the next tile's loads are in flight while this one is computed
-  for (int j = 0; j < nfull; ++j) {
-    const int cur = j & 1;
-    const bool more = j + 1 < ntiles;
-    if (more) {
-      load_tile<D>(rk, (j + 1) * kBN, row_bytes, tid, kr);
-      load_tile<D>(rv, (j + 1) * kBN, row_bytes, tid, vr);
-    }
-    attend_tile<D, false>(lds + cur * G::kKTile, lds + 2 * G::kKTile + cur * G::kVTile, qf, oacc,
-                          m_c, l_part, c, kBN, lane);
-    if (more) {
-      store_tile<D>(lds + (cur ^ 1) * G::kKTile, G::kKRow, tid, kr);
-      store_tile<D>(lds + 2 * G::kKTile + (cur ^ 1) * G::kVTile, G::kVRow, tid, vr);
-    }
+  // ---- M(0) and V(0)
+  __builtin_amdgcn_s_setprio(1);
+  m_step<D, false>(kbuf, vbuf, qf, s, p, oacc, lane);
+  __builtin_amdgcn_s_setprio(0);
+  __syncthreads();
+  vstep(0, st1, st0);
+  __syncthreads();
+  // ---- tiles 1.. in pairs, so the two register sets alternate at compile time
+  auto tile = [&](int j, Stage& to_store, Stage& to_load) {
+    if (rescale) scale_acc<D>(oacc, alpha);
+    __builtin_amdgcn_s_setprio(1);
+    m_step<D, true>(kbuf + (j & 1) * G::kKTile, vbuf + ((j - 1) & 1) * G::kVTile, qf, s, p, oacc,
+                    lane);
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
+    vstep(j, to_store, to_load);
+    __syncthreads();
+  };
+  for (int j = 1; j < ntiles; j += 2) {
+    tile(j, st0, st1);
+    if (j + 1 >= ntiles) break;
+    tile(j + 1, st1, st0);
   }
-  // the ragged last tile, keys past the segment end masked
-  if (nfull < ntiles) {
-    const int cur = nfull & 1;
-    attend_tile<D, true>(lds + cur * G::kKTile, lds + 2 * G::kKTile + cur * G::kVTile, qf, oacc,
-                         m_c, l_part, c, it.seg_len - nfull * kBN, lane);
-  }
+  // ---- M(ntiles): the last product
+  if (rescale) scale_acc<D>(oacc, alpha);
+  pv_tile<D>(vbuf + ((ntiles - 1) & 1) * G::kVTile, p, oacc, lane);
+  if (!kGroupB) __syncthreads();  // matches group B's extra barrier at the start
 
-  // ---- epilogue: O = O / l, bf16, rows past the segment end are dropped by the range check
+  // ---- epilogue: O = O / l, bf16; rows past the segment end are dropped by the range check
+  __amdgpu_buffer_rsrc_t ro = make_rsrc(o + base, seg_bytes);
   const float l_tot = half_sum(l_part);
   const float inv = 1.0f / l_tot;
 #pragma unroll
@@ -301,7 +440,18 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
 }
 
 template <int D>
-__global__ void __launch_bounds__(kThreads)
+__device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
+                                         const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+                                         __bf16* __restrict__ o, int H, float c, bool negate_q,
+                                         char* smem) {
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= kWaves / 2)
+    run_item_group<D, true>(it, q, k, v, o, H, c, negate_q, smem);
+  else
+    run_item_group<D, false>(it, q, k, v, o, H, c, negate_q, smem);
+}
+
+template <int D>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                   const __bf16* __restrict__ v, __bf16* __restrict__ o, int L, int H, int nq,
                   int total, int chunk, float c, int negate_q) {
@@ -319,7 +469,7 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
 // plan layout (int32): [0] item count, [1] error flag, then per rank r (longest segment
 // first): [2 + 2r] segment index, [3 + 2r] first item of that segment.
 template <int D>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                    const __bf16* __restrict__ v, __bf16* __restrict__ o,
                    const int32_t* __restrict__ cu, const int32_t* __restrict__ plan, int nseq,
