@@ -360,26 +360,28 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   };
   // first tile of the pair this group handles in V(j): A (K_{j+1}, V_j), B (K_{j+2}, V_{j+1})
   constexpr int kLead = kGroupB ? 1 : 0;
-  // vector step j: store the set loaded one vector step ago, load the next pair, softmax
-  auto vstep = [&](int j, Stage& to_store, Stage& to_load) {
-    store(to_store, j + 1 + kLead, j + kLead);
+  // vector step j: load the next pair, store the set loaded one vector step ago, softmax;
+  // kMasked on the ragged last tile only, so the common step is one straight block
+  auto vstep = [&](int j, Stage& to_store, Stage& to_load, auto masked) {
+    constexpr bool kMasked = decltype(masked)::value;
     load(to_load, j + 2 + kLead, j + 1 + kLead);
-    if (j + 1 < ntiles)
-      softmax_tile<false>(s, p, m_c, l_part, alpha, rescale, c, kBN, lane);
-    else
-      softmax_tile<true>(s, p, m_c, l_part, alpha, rescale, c, last_keys, lane);
-    // spread the memory operations between the softmax's VALU work
+    store(to_store, j + 1 + kLead, j + kLead);
+    softmax_tile<kMasked>(s, p, m_c, l_part, alpha, rescale, c, kMasked ? last_keys : kBN, lane);
+    // spread the memory operations between the softmax's VALU work: the loads first (they have
+    // until the next vector step to land), then the LDS writes of the older set
 #pragma unroll
     for (int i = 0; i < 2 * G::kLoads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
       __builtin_amdgcn_sched_group_barrier(0x002, 4, 3);
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * G::kLoads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 3);
       __builtin_amdgcn_sched_group_barrier(0x200, 1, 3);
     }
-#pragma unroll
-    for (int i = 0; i < 2 * G::kLoads; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 3);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
-    }
   };
+  using Full = std::false_type;
+  using Last = std::true_type;
 
   // prologue: K_0 by every thread; then the first pair(s) of this group
   load(st0, 0, 0);
@@ -399,23 +401,32 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   m_step<D, false>(kbuf, vbuf, qf, s, p, oacc, lane);
   __builtin_amdgcn_s_setprio(0);
   __syncthreads();
-  vstep(0, st1, st0);
+  if (ntiles == 1)
+    vstep(0, st1, st0, Last{});
+  else
+    vstep(0, st1, st0, Full{});
   __syncthreads();
   // ---- tiles 1.. in pairs, so the two register sets alternate at compile time
-  auto tile = [&](int j, Stage& to_store, Stage& to_load) {
+  auto tile = [&](int j, Stage& to_store, Stage& to_load, auto masked) {
     if (rescale) scale_acc<D>(oacc, alpha);
     __builtin_amdgcn_s_setprio(1);
     m_step<D, true>(kbuf + (j & 1) * G::kKTile, vbuf + ((j - 1) & 1) * G::kVTile, qf, s, p, oacc,
                     lane);
     __builtin_amdgcn_s_setprio(0);
     __syncthreads();
-    vstep(j, to_store, to_load);
+    vstep(j, to_store, to_load, masked);
     __syncthreads();
   };
-  for (int j = 1; j < ntiles; j += 2) {
-    tile(j, st0, st1);
-    if (j + 1 >= ntiles) break;
-    tile(j + 1, st1, st0);
+  int j = 1;
+  for (; j + 1 < ntiles - 1; j += 2) {  // full tiles j (odd) and j + 1
+    tile(j, st0, st1, Full{});
+    tile(j + 1, st1, st0, Full{});
+  }
+  if (j < ntiles - 1) {  // one more full tile (odd), then the last (even)
+    tile(j, st0, st1, Full{});
+    tile(j + 1, st1, st0, Last{});
+  } else if (j == ntiles - 1) {  // the last tile (odd)
+    tile(j, st0, st1, Last{});
   }
   // ---- M(ntiles): the last product
   if (rescale) scale_acc<D>(oacc, alpha);
