@@ -18,11 +18,11 @@
 //    issues the softmax VALU work, and they swap roles at each workgroup barrier.  On gfx950
 //    v_exp_f32 shares the VALU pipe with the other vector ops, while MFMAs run in the matrix
 //    core, so the softmax can hide under the other wave's matrix work.
-//  * K and V tiles of 64 keys are staged through LDS, double buffered, with padded row strides
-//    that keep the MFMA operand reads free of bank conflicts.  The global loads go through
-//    registers two sets deep and are issued only in the vector steps, spread between the
-//    softmax instructions; they are raw buffer loads whose range check returns zeros past the
-//    segment's last row.
+//  * K and V tiles of 64 keys are staged in LDS in rings of three, laid out (K padded, V
+//    XOR-swizzled) so that the MFMA operand reads are free of bank conflicts.  They arrive by
+//    LDS DMA (buffer_load ... lds), which needs no registers and no LDS write instructions,
+//    issued only in the vector steps; the raw buffer descriptor's range check returns zeros
+//    past the segment's last row.
 //  * Online softmax in the log2 domain (exp2 with scale*log2(e) folded into one FMA).  A tile
 //    is first exponentiated against the running maximum as it stands; only if some weight
 //    would exceed 2^40 (or on the first and the ragged last tile) is the tile's maximum taken
@@ -52,6 +52,7 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) void lds_void;
 
 
 constexpr int kBM = 256;       // queries per work item
@@ -61,16 +62,37 @@ constexpr int kThreads = kWaves * 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
 
+// LDS layout: a ring of three V tiles (first, so every V address fits the 16-bit immediate of a
+// DS instruction), then a ring of three K tiles; K_j and V_j sit in stage j % 3.  Tiles arrive by
+// LDS DMA (buffer_load ... lds: lane i of an instruction lands at base + 16 i), 1 KiB per
+// instruction.
+//  * K rows are padded by one 16-byte chunk (stride 2d + 16 bytes), so the 16 rows one b128 K
+//    read touches per 16 lanes fall on distinct banks.  DMA lanes that land in a pad chunk fetch
+//    a harmless duplicate.
+//  * V rows are unpadded; the 16-byte chunk c of row r is stored at chunk position c ^ vswz(r),
+//    which keeps the transposed V reads free of bank conflicts.
 template <int D>
 struct Geo {
-  static constexpr int kChunks = D / 8;                     // 16-byte chunks per row
-  static constexpr int kKRow = D * 2 + 16;                  // K row stride in LDS (bytes)
-  static constexpr int kVRow = D * 2 + 64;                  // V row stride in LDS (bytes)
+  static constexpr int kChunks = D / 8;                  // 16-byte chunks per row of d bf16
+  static constexpr int kKRow = D * 2 + 16;               // padded K row stride (bytes)
+  static constexpr int kVRow = D * 2;                    // V row stride (bytes)
   static constexpr int kKTile = kBN * kKRow;
   static constexpr int kVTile = kBN * kVRow;
-  static constexpr int kLoads = kBN * kChunks / kThreads;   // 16-byte loads per thread per tile
-  static constexpr int kLds = 2 * (kKTile + kVTile);        // double buffered
-  static_assert(kLoads >= 1 && kBN * kChunks % kThreads == 0, "tile must split evenly");
+  static constexpr int kStages = 3;
+  static constexpr int kVRing = 0;                       // byte offset of the V ring
+  static constexpr int kKRing = kStages * kVTile;        // byte offset of the K ring
+  static constexpr int kLds = kStages * (kKTile + kVTile);
+  static constexpr int kGroupWaves = kWaves / 2;
+  static constexpr int kKDma = kKTile / 1024;            // DMA instructions per K tile (17 / 9)
+  static constexpr int kVDma = kVTile / 1024;            // per V tile (16 / 8)
+  static constexpr int kKDmaMax = (kKDma + kGroupWaves - 1) / kGroupWaves;  // per wave, at most
+  static constexpr int kKDmaMin = kKDma / kGroupWaves;                      // per wave, at least
+  static constexpr int kVDmaPerWave = kVDma / kGroupWaves;
+  static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && kVDma % kGroupWaves == 0, "DMA split");
+  static_assert(kStages * kVTile <= 65536, "V addresses must fit the DS immediate");
+  __host__ __device__ static constexpr int vswz(int r) {
+    return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+  }
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
@@ -131,25 +153,44 @@ __device__ __forceinline__ void qk_tile(const lds_char* __restrict__ kt, const b
   }
 }
 
+// Lane offsets of the transposed V reads inside a V tile: for 8-row group r2 and 32-channel
+// block db, the 8 bytes of row 8 r2 + vr (+16 t) that this lane addresses.  Within each
+// 16-lane group, lane 4R + c addresses 4 channels of key row R, and after the transpose lane j
+// holds channel j of those 4 rows.
+template <int D>
+struct VOffsets {
+  int off[2][D / 32];
+  __device__ __forceinline__ explicit VOffsets(int lane) {
+    using G = Geo<D>;
+    const int g = lane >> 4, i16 = lane & 15;
+    const int vr = 4 * (g >> 1) + (i16 >> 2);        // key row inside an 8-key group
+    const int vch = 2 * (g & 1) + ((i16 & 3) >> 1);  // 16-byte chunk inside a 64-byte block
+    const int vhalf = 8 * (i16 & 1);                 // 8-byte half of that chunk
+#pragma unroll
+    for (int r2 = 0; r2 < 2; ++r2)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const int row = 8 * r2 + vr;  // the swizzle depends on the row mod 16 only
+        off[r2][db] = row * G::kVRow + (((4 * db + vch) ^ G::vswz(row)) << 4) + vhalf;
+      }
+  }
+};
+
 // O^T += V^T P^T for one 64-key tile.  p[t] holds the bf16 weights of keys
 // 16t + 8*(m/4) + 4*hb + m%4 (m = 0..7) -- the accumulator order of qk_tile -- and the V^T
-// fragments are read in that same key order with the transpose read: within each 16-lane
-// group, lane 4R + c addresses 4 channels of key row R and lane j receives channel j of 4 rows.
+// fragments are read in that same key order with the transpose read: elements 0-3 from rows
+// 16t + 4hb + 0..3, elements 4-7 from rows 16t + 8 + 4hb + 0..3.
 template <int D>
-__device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const bf16x8 (&p)[kBN / 16],
-                                        f32x16 (&o)[D / 32], int lane) {
+__device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const VOffsets<D>& vo,
+                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32]) {
   using G = Geo<D>;
-  const int g = lane >> 4, i16 = lane & 15;
-  const int vr = 4 * (g >> 1) + (i16 >> 2);     // key row inside an 8-key group
-  const int vc = 32 * (g & 1) + 8 * (i16 & 3);  // byte column inside a 64-byte channel block
-  const lds_char* vbase = vt + vr * G::kVRow + vc;
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t)
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const lds_char* va = vbase + (16 * t) * G::kVRow + db * 64;
-      bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va));
-      bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * G::kVRow));
+      const lds_char* base = vt + 16 * t * G::kVRow;
+      bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo.off[0][db]));
+      bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo.off[1][db]));
       bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
       o[db] = mfma32(a, p[t], o[db]);
     }
@@ -244,28 +285,74 @@ __device__ __forceinline__ void scale_acc(f32x16 (&o)[D / 32], float alpha) {
     for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
 }
 
+// Lane offsets (bytes, relative to the tile's first row in global memory) of one wave's share
+// of the LDS DMA of a K or a V tile.  The four waves of a group split a tile: DMA instruction
+// n = gw + 4u of the tile fills LDS bytes [1024 n, 1024 n + 1024) of it, lane i bytes
+// 1024 n + 16 i.
 template <int D>
-__device__ __forceinline__ void load_tile(__amdgpu_buffer_rsrc_t rs, int key0, int row_bytes,
-                                          int tid, u32x4 (&r)[Geo<D>::kLoads]) {
+__device__ __forceinline__ void dma_offsets_k(int gw, int lane, int row_bytes,
+                                              int* koff) {
   using G = Geo<D>;
 #pragma unroll
-  for (int u = 0; u < G::kLoads; ++u) {
-    int cidx = tid + kThreads * u;
-    int row = cidx / G::kChunks, ch = cidx % G::kChunks;
-    r[u] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + row) * row_bytes + ch * 16, 0, 0);
+  for (int u = 0; u < G::kKDmaMax; ++u) {
+    const int b = 1024 * (gw + G::kGroupWaves * u) + 16 * lane;
+    const int row = b / G::kKRow, colb = b % G::kKRow;
+    const int chunk = colb < D * 2 ? colb / 16 : 0;  // pad lanes fetch chunk 0 again
+    koff[u] = row * row_bytes + chunk * 16;
+  }
+}
+template <int D>
+__device__ __forceinline__ void dma_offsets_v(int gw, int lane, int row_bytes,
+                                              int* voff) {
+  using G = Geo<D>;
+#pragma unroll
+  for (int u = 0; u < G::kVDmaPerWave; ++u) {
+    const int b = 1024 * (gw + G::kGroupWaves * u) + 16 * lane;
+    const int row = b / G::kVRow;
+    const int chunk = ((b % G::kVRow) / 16) ^ G::vswz(row);
+    voff[u] = row * row_bytes + chunk * 16;
   }
 }
 
+// This wave's share of the DMA of the K tile whose first key is key0 (rows past the segment
+// end read as zeros through the descriptor's range check).
 template <int D>
-__device__ __forceinline__ void store_tile(lds_char* lds, int row_stride, int tid,
-                                           const u32x4 (&r)[Geo<D>::kLoads]) {
+__device__ __forceinline__ void dma_k(__amdgpu_buffer_rsrc_t rk, int key0, int row_bytes,
+                                      lds_char* tile, const int* koff, int gw) {
   using G = Geo<D>;
+  const int skip = key0 * row_bytes;
 #pragma unroll
-  for (int u = 0; u < G::kLoads; ++u) {
-    int cidx = tid + kThreads * u;
-    int row = cidx / G::kChunks, ch = cidx % G::kChunks;
-    *(lds_u32x4*)(lds + row * row_stride + ch * 16) = r[u];
+  for (int u = 0; u < G::kKDmaMax; ++u) {
+    const int n = gw + G::kGroupWaves * u;
+    if (u < G::kKDmaMin || n < G::kKDma)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(tile + 1024 * n), 16, koff[u] + skip,
+                                               0, 0, 0);
   }
+}
+template <int D>
+__device__ __forceinline__ void dma_v(__amdgpu_buffer_rsrc_t rv, int key0, int row_bytes,
+                                      lds_char* tile, const int* voff, int gw) {
+  using G = Geo<D>;
+  const int skip = key0 * row_bytes;
+#pragma unroll
+  for (int u = 0; u < G::kVDmaPerWave; ++u)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(tile + 1024 * (gw + G::kGroupWaves * u)),
+                                             16, voff[u] + skip, 0, 0, 0);
+}
+
+// Waits until at most N of this wave's vector-memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);  // gfx9 encoding: expcnt and lgkmcnt left open
+}
+
+// Workgroup barrier without a memory fence (the waits before it are explicit); the empty asm
+// statements keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void block_sync() {
+  __asm__ volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  __asm__ volatile("" ::: "memory");
 }
 
 // The matrix step of tile j: S_j = K_j Q^T followed by O += V_{j-1} P_{j-1}, in one basic
@@ -273,10 +360,11 @@ __device__ __forceinline__ void store_tile(lds_char* lds, int row_stride, int ti
 // MFMAs earlier: 8 K reads up front, then one MFMA followed by the next one or two operand reads.
 template <int D, bool kPV>
 __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
-                                       const bf16x8 (&qf)[D / 16], f32x16 (&s)[kBN / 32],
-                                       const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32], int lane) {
+                                       const VOffsets<D>& vo, const bf16x8 (&qf)[D / 16],
+                                       f32x16 (&s)[kBN / 32], const bf16x8 (&p)[kBN / 16],
+                                       f32x16 (&o)[D / 32], int lane) {
   qk_tile<D>(kt, qf, s, lane);
-  if (kPV) pv_tile<D>(vt, p, o, lane);
+  if (kPV) pv_tile<D>(vt, vo, p, o);
   constexpr int kQK = (kBN / 32) * (D / 16);          // MFMAs of S (16 at d = 128)
   constexpr int kPVm = kPV ? (kBN / 16) * (D / 32) : 0;  // MFMAs of PV (16 at d = 128)
   constexpr int kAhead = 8;
@@ -301,14 +389,15 @@ __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const ld
 // work.  The matrix step raises its wave priority so its MFMAs issue first, and it does no
 // global-memory work at all.
 //
-// K/V staging: each thread moves a fixed share of every tile's 16-byte chunks through
-// registers, two register sets deep, in its vector steps only, spread between the softmax
-// instructions: in V(j) it writes the set loaded in V(j-1) to LDS and loads the next tile into
-// the other set.  Group A handles (K_{j+1}, V_j) in V(j), group B (K_{j+2}, V_{j+1}); both halves
-// of (K_m, V_{m-1}) are in LDS before group A's M(m), and no buffer is rewritten before both
-// groups have read it (K_m and V_m in buffer m % 2).  Loads of tiles past the segment end read
-// zeros and their writes land in a buffer nobody reads any more, so the schedule has no branches.
-// The two groups are separate instantiations, so each has a straight-line schedule.
+// K/V staging is by LDS DMA, issued in the vector steps only: group A fetches K_{j+2} in V(j),
+// group B fetches V_{j+2}, and each wave waits for the fetch of its previous vector step right
+// before the barrier that closes V(j).  Phases (A's M(j) = 2j, A's V(j) = B's M(j) = 2j + 1,
+// B's V(j) = 2j + 2): K_m is complete before phase 2m, where A's M(m) first reads it, and
+// V_{m-1} before phase 2m; a stage is refilled only after the barrier that follows its last
+// reader (B's M(m) at 2m + 1 for K_m, B's M(m + 1) at 2m + 3 for V_m), so three stages suffice.
+// Fetches past the segment end read zeros and land in stages nobody reads any more, so the
+// schedule has no branches.  The two groups are separate instantiations, so each has a
+// straight-line schedule.
 template <int D, bool kGroupB>
 __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __restrict__ q,
                                                const __bf16* __restrict__ k,
@@ -317,6 +406,7 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   using G = Geo<D>;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int gw = wave & (G::kGroupWaves - 1);  // wave inside its group
   const int hb = lane >> 5, col = lane & 31;
   const int row_bytes = H * D * 2;
   const int64_t base = (it.seg_start * H + it.h) * D;  // element offset of (first token, h)
@@ -325,8 +415,18 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, seg_bytes);
   __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, seg_bytes);
   lds_char* const lds = (lds_char*)smem;
-  lds_char* const kbuf = lds;                  // 2 x kKTile
-  lds_char* const vbuf = lds + 2 * G::kKTile;  // 2 x kVTile
+  auto ktile = [&](int stage) { return lds + G::kKRing + stage * G::kKTile; };
+  auto vtile = [&](int stage) { return lds + G::kVRing + stage * G::kVTile; };
+  const VOffsets<D> vo(lane);
+  int koff[G::kKDmaMax], voff[G::kVDmaPerWave];
+  if (!kGroupB) dma_offsets_k<D>(gw, lane, row_bytes, koff);
+  else dma_offsets_v<D>(gw, lane, row_bytes, voff);
+  // this group's fetch of tile j (K for group A, V for group B) into stage j % 3
+  auto fetch = [&](int j, int stage) {
+    if (!kGroupB) dma_k<D>(rk, j * kBN, row_bytes, ktile(stage), koff, gw);
+    else dma_v<D>(rv, j * kBN, row_bytes, vtile(stage), voff, gw);
+  };
+  constexpr int kFetchWait = kGroupB ? G::kVDmaPerWave : G::kKDmaMin;  // fewest per wave
 
   // Q fragments (B operand of S^T = K Q^T): query col of this wave, channels 16kk + 8hb + 0..7
   const int qrow = it.q_begin + 32 * wave + col;
@@ -348,90 +448,58 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
 
   const int ntiles = (it.seg_len + kBN - 1) / kBN;
   const int last_keys = it.seg_len - (ntiles - 1) * kBN;  // valid keys of the last tile
-  struct Stage { u32x4 k[G::kLoads], v[G::kLoads]; };
-  Stage st0, st1;
-  auto load = [&](Stage& x, int kj, int vj) {
-    load_tile<D>(rk, kj * kBN, row_bytes, tid, x.k);
-    load_tile<D>(rv, vj * kBN, row_bytes, tid, x.v);
-  };
-  auto store = [&](const Stage& x, int kj, int vj) {
-    store_tile<D>(kbuf + (kj & 1) * G::kKTile, G::kKRow, tid, x.k);
-    store_tile<D>(vbuf + (vj & 1) * G::kVTile, G::kVRow, tid, x.v);
-  };
-  // first tile of the pair this group handles in V(j): A (K_{j+1}, V_j), B (K_{j+2}, V_{j+1})
-  constexpr int kLead = kGroupB ? 1 : 0;
-  // vector step j: load the next pair, store the set loaded one vector step ago, softmax;
-  // kMasked on the ragged last tile only, so the common step is one straight block
-  auto vstep = [&](int j, Stage& to_store, Stage& to_load, auto masked) {
+  // vector step j: fetch tile j + 2 into stage st2, softmax S_j -> P_j, wait for the fetch of
+  // the previous vector step, barrier; kMasked on the ragged last tile only
+  auto vstep = [&](int j, int st2, auto masked) {
     constexpr bool kMasked = decltype(masked)::value;
-    load(to_load, j + 2 + kLead, j + 1 + kLead);
-    store(to_store, j + 1 + kLead, j + kLead);
+    fetch(j + 2, st2);
     softmax_tile<kMasked>(s, p, m_c, l_part, alpha, rescale, c, kMasked ? last_keys : kBN, lane);
-    // spread the memory operations between the softmax's VALU work: the loads first (they have
-    // until the next vector step to land), then the LDS writes of the older set
 #pragma unroll
-    for (int i = 0; i < 2 * G::kLoads; ++i) {
+    for (int i = 0; i < G::kKDmaMax; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 3);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 3);
     }
-#pragma unroll
-    for (int i = 0; i < 2 * G::kLoads; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 3);
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 3);
-    }
+    wait_vmem<kFetchWait>();
+    block_sync();
   };
   using Full = std::false_type;
   using Last = std::true_type;
 
-  // prologue: K_0 by every thread; then the first pair(s) of this group
-  load(st0, 0, 0);
-  store_tile<D>(kbuf, G::kKRow, tid, st0.k);
-  if (kGroupB) {
-    load(st0, 1, 0);      // (K_1, V_0), written right away
-    store(st0, 1, 0);
-    load(st1, 2, 1);      // (K_2, V_1), written in V(0)
-  } else {
-    load(st1, 1, 0);      // (K_1, V_0), written in V(0)
-  }
-  __syncthreads();
-  if (kGroupB) __syncthreads();  // group B starts one step behind
+  // prologue: tiles 0 and 1 of this group's operand, complete before anyone reads them
+  fetch(0, 0);
+  fetch(1, 1);
+  wait_vmem<0>();
+  block_sync();
+  if (kGroupB) block_sync();  // group B starts one step behind
 
   // ---- M(0) and V(0)
   __builtin_amdgcn_s_setprio(1);
-  m_step<D, false>(kbuf, vbuf, qf, s, p, oacc, lane);
+  m_step<D, false>(ktile(0), vtile(0), vo, qf, s, p, oacc, lane);
   __builtin_amdgcn_s_setprio(0);
-  __syncthreads();
+  block_sync();
   if (ntiles == 1)
-    vstep(0, st1, st0, Last{});
+    vstep(0, 2, Last{});
   else
-    vstep(0, st1, st0, Full{});
-  __syncthreads();
-  // ---- tiles 1.. in pairs, so the two register sets alternate at compile time
-  auto tile = [&](int j, Stage& to_store, Stage& to_load, auto masked) {
+    vstep(0, 2, Full{});
+  // ---- tiles 1..: stage of tile j is sj = j % 3; V_{j-1} sits in (j + 2) % 3
+  int s0 = 1, s1 = 2, s2 = 0;  // (j, j + 1, j + 2) % 3 for j = 1
+  auto tile = [&](int j, auto masked) {
     if (rescale) scale_acc<D>(oacc, alpha);
     __builtin_amdgcn_s_setprio(1);
-    m_step<D, true>(kbuf + (j & 1) * G::kKTile, vbuf + ((j - 1) & 1) * G::kVTile, qf, s, p, oacc,
-                    lane);
+    m_step<D, true>(ktile(s0), vtile(s2), vo, qf, s, p, oacc, lane);
     __builtin_amdgcn_s_setprio(0);
-    __syncthreads();
-    vstep(j, to_store, to_load, masked);
-    __syncthreads();
+    block_sync();
+    vstep(j, s2, masked);
+    const int t = s0; s0 = s1; s1 = s2; s2 = t;
   };
   int j = 1;
-  for (; j + 1 < ntiles - 1; j += 2) {  // full tiles j (odd) and j + 1
-    tile(j, st0, st1, Full{});
-    tile(j + 1, st1, st0, Full{});
-  }
-  if (j < ntiles - 1) {  // one more full tile (odd), then the last (even)
-    tile(j, st0, st1, Full{});
-    tile(j + 1, st1, st0, Last{});
-  } else if (j == ntiles - 1) {  // the last tile (odd)
-    tile(j, st0, st1, Last{});
-  }
-  // ---- M(ntiles): the last product
+  for (; j < ntiles - 1; ++j) tile(j, Full{});
+  if (j == ntiles - 1) tile(j, Last{});
+  // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = s2 now
   if (rescale) scale_acc<D>(oacc, alpha);
-  pv_tile<D>(vbuf + ((ntiles - 1) & 1) * G::kVTile, p, oacc, lane);
-  if (!kGroupB) __syncthreads();  // matches group B's extra barrier at the start
+  pv_tile<D>(vtile(s2), vo, p, oacc);
+  if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
+  wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
 
   // ---- epilogue: O = O / l, bf16; rows past the segment end are dropped by the range check
   __amdgpu_buffer_rsrc_t ro = make_rsrc(o + base, seg_bytes);
