@@ -25,9 +25,13 @@
  * Rows are independent, so callers may ask for any subset of (token, head) rows; the row loop
  * is an OpenMP parallel for.
  *
- * Parity pins (tests/test_oracle.py): mpmath brute force at 50 digits, torch's CPU float64
- * scaled_dot_product_attention per segment, closed forms (one key, two keys, identical keys,
- * constant V, dominant key), invariants (shift, permutation, segment independence, convex hull).
+ * A second entry point computes chunk queries against per-session key/value ranges with
+ * the log-sum-exp of every row (defined above ts_ref_attn_kv_rows_bf16).
+ *
+ * Parity pins (tests/test_oracle.py, tests/test_oracle_kv.py): mpmath brute force at 50
+ * digits, torch's CPU float64 scaled_dot_product_attention per segment, scipy's logsumexp,
+ * closed forms (one key, two keys, identical keys, constant V, dominant key), invariants (shift,
+ * permutation, segment independence, convex hull, merging two key ranges by their lse).
  */
 #include <math.h>
 #include <stdint.h>
@@ -180,6 +184,116 @@ int ts_ref_attn_weights_f64(const double* q, const double* k, const double* v,
   attend_row(tq, tk, tv, cu_seqlens, nseq, H, d, scale, t, h, z, out, weights);
   free(z);
   return REF_OK;
+}
+
+/*
+ * Chunk queries against per-session key/value ranges, with the log-sum-exp of every row.
+ *
+ * A chunk-autoregressive streaming model generates each new chunk conditioned on the cached
+ * state of the session's earlier chunks (Sec. 2, "Streaming video generation workflow"); that
+ * cache is part of the session's isolated state region (Sec. 6.1, "Session memory layout"), and
+ * one model call serves the coalesced batch of ready sessions (Sec. 3.1).  Segment s of such a
+ * batch has its queries at rows [cu_q[s], cu_q[s+1]) of Q and its keys and values at rows
+ * [cu_k[s], cu_k[s+1]) of K and V -- typically the session's cached tokens followed by the
+ * chunk's own -- and every query attends to every key of its segment.  For query row t of
+ * segment s, head h and channel c:
+ *     z_j      = scale * sum_{c'} Q[t,h,c'] * K[j,h,c']     for j in [cu_k[s], cu_k[s+1])
+ *     m        = max_j z_j
+ *     lse      = m + log(sum_j exp(z_j - m))                (= log sum_j exp z_j)
+ *     O[t,h,c] = sum_j exp(z_j - m) V[j,h,c] / sum_j exp(z_j - m)
+ * A segment without keys has the empty sum: O = 0 and lse = -inf.  With cu_q == cu_k this is
+ * the self-attention above.  Same arithmetic rules: double, libm exp/log, left-to-right sums.
+ */
+static void attend_kv_row(tensor_t q, tensor_t k, tensor_t v, const int32_t* cu_q,
+                          const int32_t* cu_k, int32_t nseq, int32_t H, int32_t d, double scale,
+                          int64_t t, int32_t h, double* z, double* out, double* lse) {
+  int32_t s = find_segment(cu_q, nseq, t);
+  int64_t kb = cu_k[s], ke = cu_k[s + 1];
+  int64_t row_stride = (int64_t)H * d;
+  int64_t qrow = t * row_stride + (int64_t)h * d;
+  for (int32_t c = 0; c < d; c++) out[c] = 0.0;
+  if (ke == kb) {
+    *lse = -INFINITY;
+    return;
+  }
+  /* scores and their maximum */
+  double m = -INFINITY;
+  for (int64_t j = kb; j < ke; j++) {
+    int64_t krow = j * row_stride + (int64_t)h * d;
+    double dot = 0.0;
+    for (int32_t c = 0; c < d; c++) dot += elem(q, qrow + c) * elem(k, krow + c);
+    z[j - kb] = scale * dot;
+    if (z[j - kb] > m) m = z[j - kb];
+  }
+  /* unnormalised weights, their sum, the weighted sum of V rows */
+  double den = 0.0;
+  for (int64_t j = kb; j < ke; j++) {
+    double w = exp(z[j - kb] - m);
+    den += w;
+    int64_t vrow = j * row_stride + (int64_t)h * d;
+    for (int32_t c = 0; c < d; c++) out[c] += w * elem(v, vrow + c);
+  }
+  for (int32_t c = 0; c < d; c++) out[c] = out[c] / den;
+  *lse = m + log(den);
+}
+
+static int attn_kv_rows(tensor_t q, tensor_t k, tensor_t v, const int32_t* cu_q,
+                        const int32_t* cu_k, int32_t nseq, int32_t H, int32_t d, double scale,
+                        const int64_t* row_t, const int32_t* row_h, int64_t nrows, double* out,
+                        double* lse) {
+  if (!cu_q || !cu_k || !out || !lse || nseq < 1 || H < 1 || d < 1 || nrows < 0)
+    return REF_ERR_ARG;
+  if ((nrows > 0) && (!row_t || !row_h)) return REF_ERR_ARG;
+  int rc = check_segments(cu_q, nseq);
+  if (rc) return rc;
+  rc = check_segments(cu_k, nseq);
+  if (rc) return rc;
+  int64_t Tq = cu_q[nseq];
+  int32_t maxlen = 0;
+  for (int32_t s = 0; s < nseq; s++)
+    if (cu_k[s + 1] - cu_k[s] > maxlen) maxlen = cu_k[s + 1] - cu_k[s];
+  for (int64_t r = 0; r < nrows; r++)
+    if (row_t[r] < 0 || row_t[r] >= Tq || row_h[r] < 0 || row_h[r] >= H) return REF_ERR_ROW;
+
+  int failed = 0;
+#pragma omp parallel
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)(maxlen > 0 ? maxlen : 1));
+    if (!z) {
+#pragma omp atomic write
+      failed = 1;
+    }
+#pragma omp for schedule(dynamic, 4)
+    for (int64_t r = 0; r < nrows; r++) {
+      if (z)
+        attend_kv_row(q, k, v, cu_q, cu_k, nseq, H, d, scale, row_t[r], row_h[r], z, out + r * d,
+                      lse + r);
+    }
+    free(z);
+  }
+  return failed ? REF_ERR_NOMEM : REF_OK;
+}
+
+/* Rows (token row_t[r] of q, head row_h[r]) of chunk-vs-cache attention from bf16 inputs:
+ * q is [Tq][H][d] with Tq = cu_q[nseq], k and v are [Tk][H][d] with Tk = cu_k[nseq].
+ * out is [nrows][d], lse is [nrows]. */
+int ts_ref_attn_kv_rows_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                             const int32_t* cu_q, const int32_t* cu_k, int32_t nseq, int32_t H,
+                             int32_t d, double scale, const int64_t* row_t, const int32_t* row_h,
+                             int64_t nrows, double* out, double* lse) {
+  if (!q || !k || !v) return REF_ERR_ARG;
+  tensor_t tq = {NULL, q}, tk = {NULL, k}, tv = {NULL, v};
+  return attn_kv_rows(tq, tk, tv, cu_q, cu_k, nseq, H, d, scale, row_t, row_h, nrows, out, lse);
+}
+
+/* Same, from double inputs. */
+int ts_ref_attn_kv_rows_f64(const double* q, const double* k, const double* v,
+                            const int32_t* cu_q, const int32_t* cu_k, int32_t nseq, int32_t H,
+                            int32_t d, double scale, const int64_t* row_t, const int32_t* row_h,
+                            int64_t nrows, double* out, double* lse) {
+  if (!q || !k || !v) return REF_ERR_ARG;
+  tensor_t tq = {q, NULL}, tk = {k, NULL}, tv = {v, NULL};
+  return attn_kv_rows(tq, tk, tv, cu_q, cu_k, nseq, H, d, scale, row_t, row_h, nrows, out, lse);
 }
 
 /* Number of OpenMP threads a parallel region of the oracle uses. */

@@ -56,3 +56,20 @@ def test_sample_rows_cover_segment_ends_for_every_head():
     assert rt.min() >= 0 and rt.max() < w.T
     rt2, _ = W.sample_rows(w)
     assert np.array_equal(rt, rt2)
+
+
+def test_kv_workloads_shapes_and_draws():
+    for w in W.KV_WORKLOADS.values():
+        assert len(w.q_seqlens) == len(w.k_seqlens)
+        assert w.cu_q[-1] == w.Tq and w.cu_k[-1] == w.Tk
+        assert all(b >= a for a, b in zip(w.q_seqlens, w.k_seqlens))  # keys include the chunk
+        assert w.flops == sum(4 * a * b * w.d * w.H for a, b in zip(w.q_seqlens, w.k_seqlens))
+    w = W.KvWorkload("t", (5, 0, 9), (20, 3, 9), 2, 64, 3, True)
+    q, k, v = W.make_kv_inputs(w)
+    assert q.shape == (14, 2, 64) and k.shape == v.shape == (32, 2, 64)
+    assert q.dtype == k.dtype == v.dtype == torch.bfloat16
+    q2, k2, v2 = W.make_kv_inputs(w)
+    assert torch.equal(q, q2) and torch.equal(k, k2) and torch.equal(v, v2)
+    row_t, row_h = W.sample_kv_rows(w, n_random=4)
+    assert set(row_t.tolist()) >= {0, 4, 5, 13} and row_t.max() < w.Tq
+    assert row_h.max() == 1

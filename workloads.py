@@ -8,6 +8,9 @@ inputs of such a model:
     75600 tokens = 21 x 45 x 80 (720p-class); tokens are flattened frame-major.
   * 12 and 40 heads of width 128: a ~1.3B-class and a large video DiT.
   * The packed case is one coalesced chunk batch of six sessions (paper Sec. 3.1).
+  * The chunk-vs-cache cases model the per-chunk step of a chunk-autoregressive model: each
+    session's new chunk (queries) attends to its cached frames followed by the chunk itself
+    (keys/values), paper Sec. 2 and Sec. 6.1; 1560 tokens = one 30 x 52 latent frame.
   * Q, V ~ N(0, 1); K ~ N(0, 1) plus, for the DiT shapes, one offset per (head, channel) drawn
     from N(0, 2) (variance 2) to mimic channel outliers.  Draws are float32 from one CPU
     torch.Generator seeded with the workload number, in the order q, k, v, offset, then rounded
@@ -84,6 +87,100 @@ def make_inputs(w, seed=None):
     k = k32.to(torch.bfloat16)
     del k32
     return q, k, v
+
+
+@dataclass(frozen=True)
+class KvWorkload:
+    """Chunk queries against per-session key/value ranges: segment s has q_seqlens[s] queries and
+    k_seqlens[s] keys (the session's cached tokens followed by the chunk's own)."""
+    name: str
+    q_seqlens: tuple
+    k_seqlens: tuple
+    H: int
+    d: int
+    seed: int
+    k_offset: bool = False
+    note: str = field(default="", compare=False)
+
+    @property
+    def Tq(self):
+        return int(sum(self.q_seqlens))
+
+    @property
+    def Tk(self):
+        return int(sum(self.k_seqlens))
+
+    @property
+    def cu_q(self):
+        return np.concatenate([[0], np.cumsum(self.q_seqlens)]).astype(np.int32)
+
+    @property
+    def cu_k(self):
+        return np.concatenate([[0], np.cumsum(self.k_seqlens)]).astype(np.int32)
+
+    @property
+    def max_q(self):
+        return int(max(self.q_seqlens)) if self.q_seqlens else 0
+
+    @property
+    def max_k(self):
+        return int(max(self.k_seqlens)) if self.k_seqlens else 0
+
+    @property
+    def flops(self):
+        """Algorithmic flops of one call: sum_s 4 Lq_s Lk_s d H."""
+        return sum(4 * int(a) * int(b) * self.d * self.H for a, b in zip(self.q_seqlens, self.k_seqlens))
+
+    @property
+    def hbm_bytes(self):
+        """Algorithmic HBM bytes: Q read and O written (Tq rows), K and V read (Tk rows), bf16."""
+        return 2 * (self.Tq + self.Tk) * self.H * self.d * 2
+
+    @property
+    def scale(self):
+        return float(np.float32(1.0) / np.sqrt(np.float32(self.d)))
+
+
+FRAME = 30 * 52  # tokens of one latent frame
+KV_WORKLOADS = {
+    "kv_chunk": KvWorkload("kv_chunk", (3 * FRAME,) * 5, tuple((c + 3) * FRAME for c in (6, 9, 12, 15, 18)),
+                           40, 128, 6, True,
+                           note="5 sessions: 3-frame chunks (4680 queries) vs 6-18 cached frames + the "
+                                "chunk (14040-32760 keys), H=40, d=128"),
+    "kv_chunk_1s": KvWorkload("kv_chunk_1s", (FRAME,), (21 * FRAME,), 12, 128, 7, True,
+                              note="1 session: a 1-frame chunk (1560 queries) vs 20 cached frames + "
+                                   "the chunk (32760 keys), H=12, d=128"),
+}
+
+
+def make_kv_inputs(w, seed=None):
+    """(q [Tq, H, d], k [Tk, H, d], v [Tk, H, d]) bf16 CPU tensors, drawn like make_inputs."""
+    g = torch.Generator().manual_seed(w.seed if seed is None else seed)
+    q = torch.randn((w.Tq, w.H, w.d), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    k32 = torch.randn((w.Tk, w.H, w.d), generator=g, dtype=torch.float32)
+    v = torch.randn((w.Tk, w.H, w.d), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    if w.k_offset:
+        offset = torch.randn((w.H, w.d), generator=g, dtype=torch.float32) * float(np.sqrt(2.0))
+        k32 += offset
+    k = k32.to(torch.bfloat16)
+    del k32
+    return q, k, v
+
+
+def sample_kv_rows(w, n_random=64, seed=None):
+    """(row_t, row_h) over the query rows: for every head, the first and last query of every
+    segment with queries plus n_random seeded random ones (seed 100 + workload seed)."""
+    rng = np.random.default_rng(100 + w.seed if seed is None else seed)
+    cu = w.cu_q
+    ts = []
+    for s in range(len(w.q_seqlens)):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        if hi <= lo:
+            continue
+        ts.extend([lo, hi - 1])
+        ts.extend(rng.integers(lo, hi, size=n_random).tolist())
+    ts = np.asarray(ts, dtype=np.int64)
+    return np.tile(ts, w.H), np.repeat(np.arange(w.H, dtype=np.int32), ts.size)
 
 
 def bf16_bits(t):
