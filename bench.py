@@ -10,6 +10,10 @@ Prints one JSON line:
                 kernel source (null when the kernel source changed since)
   cpu_baseline  the fp64 oracle timed on this host's cores on a bounded row sample of the same
                 workload, in the same unit; the sampled rows also serve as a parity check
+Other workloads (--workload): the dense and packed self-attention cases of workloads.WORKLOADS,
+and the chunk-vs-cache cases of workloads.KV_WORKLOADS (ts_attn_fwd_kvcache with the library's
+automatic key splits: flops = sum_s 4 Lq_s Lk_s d H; the events bracket the whole call, i.e. the
+planning, attention and, when split, merge kernels).
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--cpu-seconds S]
 """
 import argparse
@@ -54,19 +58,27 @@ def cpu_baseline(w, q, k, v, o_gpu, seconds):
     from oracle import ts_ref
 
     ts_ref.load()
-    row_t, row_h = W.sample_rows(w, n_random=4096, seed=999)
+    kv = isinstance(w, W.KvWorkload)
+    if kv:
+        row_t, row_h = W.sample_kv_rows(w, n_random=4096, seed=999)
+    else:
+        row_t, row_h = W.sample_rows(w, n_random=4096, seed=999)
     perm = np.random.default_rng(7).permutation(row_t.size)
     row_t, row_h = row_t[perm], row_h[perm]
     qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
-    cu = w.cu_seqlens
-    seg_len = np.diff(cu)
+    cu = w.cu_q if kv else w.cu_seqlens
+    seg_len = np.diff(w.cu_k) if kv else np.diff(cu)  # keys each row attends to
     seg_of = np.searchsorted(cu, row_t, side="right") - 1
     done, flops, t_total, batch = 0, 0.0, 0.0, 64
     refs = []
     while t_total < seconds and done < row_t.size:
         sl = slice(done, min(done + batch, row_t.size))
         t0 = time.perf_counter()
-        refs.append(ts_ref.attn_rows(qb, kb, vb, cu, w.scale, row_t[sl], row_h[sl]))
+        if kv:
+            refs.append(ts_ref.attn_kv_rows(qb, kb, vb, w.cu_q, w.cu_k, w.scale, row_t[sl],
+                                            row_h[sl])[0])
+        else:
+            refs.append(ts_ref.attn_rows(qb, kb, vb, cu, w.scale, row_t[sl], row_h[sl]))
         t_total += time.perf_counter() - t0
         flops += float(np.sum(4.0 * seg_len[seg_of[sl]] * w.d))
         done = sl.stop
@@ -125,15 +137,21 @@ def main():
                           "GB/s_read_plus_write": 2 * src.numel() * 2 / dt / 1e9}), flush=True)
         return
 
-    w = W.WORKLOADS[args.workload]
-    q, k, v = W.make_inputs(w)
+    kv = args.workload in W.KV_WORKLOADS
+    w = W.KV_WORKLOADS[args.workload] if kv else W.WORKLOADS[args.workload]
+    q, k, v = W.make_kv_inputs(w) if kv else W.make_inputs(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
-    cu = torch.tensor(w.cu_seqlens, device=dev)
-    dense = len(w.seqlens) == 1
+    if kv:
+        cuq, cuk = torch.tensor(w.cu_q, device=dev), torch.tensor(w.cu_k, device=dev)
+    else:
+        cu = torch.tensor(w.cu_seqlens, device=dev)
+    dense = not kv and len(w.seqlens) == 1
     out = torch.empty_like(qd)
 
     def step():
-        if dense:
+        if kv:
+            ts.ts_attn_fwd_kvcache(qd, kd, vd, cuq, cuk, w.max_q, w.max_k, out=out)
+        elif dense:
             ts.ts_attn_fwd(qd.view(1, w.T, w.H, w.d), kd.view(1, w.T, w.H, w.d),
                            vd.view(1, w.T, w.H, w.d), out=out.view(1, w.T, w.H, w.d))
         else:
@@ -173,7 +191,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "segments": list(w.seqlens), "T": w.T, "H": w.H, "d": w.d,
+        "config": {"workload": w.name,
+                   **({"query_segments": list(w.q_seqlens), "key_segments": list(w.k_seqlens),
+                       "Tq": w.Tq, "Tk": w.Tk} if kv else {"segments": list(w.seqlens), "T": w.T}),
+                   "H": w.H, "d": w.d,
                    "causal": False, "flops_per_call": w.flops, "hbm_bytes_per_call": w.hbm_bytes,
                    "kernel_ms_mean": kernel_ms, "kernel_ms_min": float(np.min(launch_ms)),
                    "kernel_ms_max": float(np.max(launch_ms)),

@@ -20,7 +20,8 @@
  *  - Tensors q, k, v, o: device pointers to bfloat16, contiguous, token-major [T][H][d]
  *    (row stride H*d elements).  For the dense call T = B*L, i.e. [B][L][H][d].
  *    Base pointers must be 16-byte aligned.  d must be 64 or 128.
- *  - o must not overlap q, k or v (they may overlap each other).
+ *  - o must not overlap q, k or v (they may overlap each other).  For chunk-vs-cache calls
+ *    q/o have total_q rows and k/v total_k rows.
  *  - scale: any finite float (0 is allowed: O becomes the segment mean of V).  Typical:
  *    1/sqrt(d) rounded to float.
  *  - stream: a hipStream_t passed as void* (NULL = the legacy default stream).  Calls are
@@ -37,7 +38,8 @@
  *  - Thread safety: all entry points may be called concurrently from several host threads.
  *  - Size limits: (L or max_seqlen + 256) * H * d * 2 bytes must stay below 2^31, and the
  *    work items (H * ceil(L / 256) per sequence; H * (ceil(T / 256) + nseq) for packed
- *    batches) below 2^23.  Larger problems return TS_ERR_SHAPE.
+ *    batches; 16 * H * (ceil(total_q / 256) + nseq) for chunk-vs-cache calls) below 2^23.
+ *    Larger problems return TS_ERR_SHAPE.
  */
 #ifndef TS_ATTN_H
 #define TS_ATTN_H
@@ -48,7 +50,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 1
+#define TS_ATTN_ABI_VERSION 2
 
 typedef enum ts_status {
   TS_OK = 0,
@@ -93,6 +95,46 @@ int ts_attn_fwd(const void* q, const void* k, const void* v, void* o, int32_t B,
 int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
                        const int32_t* cu_seqlens, int32_t nseq, int32_t max_seqlen,
                        int32_t total_tokens, int32_t H, int32_t d, float scale, void* stream);
+
+/*
+ * Chunk queries against per-session key/value caches, with an optional log-sum-exp output.
+ * The streaming models the paper serves generate each new chunk of a session conditioned on
+ * the cached state of its earlier chunks (Sec. 2, "Streaming video generation workflow"); that
+ * state, the KV cache among it, lives in the session's isolated region (Sec. 6.1, "Session
+ * memory layout"), and one model call serves the coalesced batch of ready sessions (Sec. 3.1).
+ * Segment s of the call has
+ *   queries  rows [cu_seqlens_q[s], cu_seqlens_q[s+1]) of q and o   (the session's new chunk)
+ *   keys     rows [cu_seqlens_k[s], cu_seqlens_k[s+1]) of k and v   (typically its cached
+ *            tokens followed by the chunk's own),
+ * and every query attends to every key of its segment:
+ *   O[t,h,c] = sum_j softmax_j(scale * <Q[t,h,:], K[j,h,:]>) * V[j,h,c]
+ *   lse[t,h] = ln sum_j exp(scale * <Q[t,h,:], K[j,h,:]>)
+ * A segment with queries but no keys gets O = 0 and lse = -inf.  With cu_seqlens_q ==
+ * cu_seqlens_k (same tensors for q and k rows) it is the packed self-attention above.
+ *  q, o            bf16 [total_q][H][d];  k, v  bf16 [total_k][H][d]  (DEVICE, 16-byte aligned)
+ *  lse             DEVICE float32 [total_q][H] (4-byte aligned), or NULL to skip it
+ *  cu_seqlens_q/k  DEVICE int32, nseq+1 entries each: start at 0, nondecreasing, end at
+ *                  total_q / total_k.  Empty segments are allowed on either side.
+ *  max_seqlen_q/k  upper bounds of the segment lengths (host values; size the launch)
+ *  num_splits      0: chosen by the library.  n in 1..16: every (segment, head, 256-query tile)
+ *                  is split into n consecutive key ranges run by separate workgroups, and a
+ *                  second kernel merges their results by their log-sum-exp.  Splitting fills
+ *                  the GPU when there are few query tiles (short chunks, long caches).  The
+ *                  result of a split call agrees with n = 1 to float32 rounding of the partial
+ *                  results, not bit for bit; n = 1 is bit-identical to ts_attn_fwd_varlen when
+ *                  the offsets coincide.
+ * o must not overlap q, k or v, and lse must not overlap any of q, k, v, o (TS_ERR_ALIAS).
+ * Device memory: the plan and, for n > 1, float32 partial results (n * total_q * H * (d + 1)
+ * floats) come from a stream-ordered pool allocation made and released by the call
+ * (TS_ERR_NOMEM if it cannot be made).  Bad offsets behave as in ts_attn_fwd_varlen (a device
+ * no-op, or TS_ERR_SEGMENTS under TS_ATTN_VALIDATE=1).  num_splits outside 0..16 and the size
+ * limits above (for max_seqlen_q and max_seqlen_k each) give TS_ERR_SHAPE.
+ */
+int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, float* lse,
+                        const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int32_t nseq,
+                        int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
+                        int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits,
+                        void* stream);
 
 /* Human-readable name of a ts_status value (a static string; never NULL). */
 const char* ts_attn_status_str(int status);

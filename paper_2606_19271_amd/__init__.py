@@ -3,7 +3,8 @@
 The compute lives in libts_attn.so (hand-written HIP kernels behind the C ABI of
 include/ts_attn.h); this package only marshals torch tensors into that ABI.
 """
-from .attention import ts_attn_fwd, ts_attn_fwd_varlen, default_scale  # noqa: F401
+from .attention import (ts_attn_fwd, ts_attn_fwd_kvcache, ts_attn_fwd_varlen,  # noqa: F401
+                        default_scale)
 from ._lib import TsAttnError, load, status_str  # noqa: F401
 
 

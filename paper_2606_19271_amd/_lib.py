@@ -34,6 +34,8 @@ def load():
     lib.ts_attn_fwd.restype = ctypes.c_int
     lib.ts_attn_fwd_varlen.argtypes = [p, p, p, p, p, i32, i32, i32, i32, i32, f32, p]
     lib.ts_attn_fwd_varlen.restype = ctypes.c_int
+    lib.ts_attn_fwd_kvcache.argtypes = [p, p, p, p, p, p, p] + [i32] * 7 + [f32, i32, p]
+    lib.ts_attn_fwd_kvcache.restype = ctypes.c_int
     lib.ts_attn_status_str.argtypes = [ctypes.c_int]
     lib.ts_attn_status_str.restype = ctypes.c_char_p
     lib.ts_attn_abi_version.argtypes = []

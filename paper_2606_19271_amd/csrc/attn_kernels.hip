@@ -114,13 +114,36 @@ __device__ __forceinline__ float half_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// One work item: queries [q_begin, q_begin + kBM) of a segment, head h.
+// One work item: queries [q_begin, q_begin + kBM) of a segment, head h, against the 64-key
+// tiles [tile_begin, tile_begin + ntiles) of the segment's keys.  For self-attention the query
+// and key rows of a segment coincide; for chunk queries against a session's cache they are
+// separate ranges of q/o and of k/v.
 struct Item {
-  int64_t seg_start;  // first token of the segment
-  int seg_len;        // tokens in the segment
-  int h;              // head
-  int q_begin;        // first query of the tile, relative to the segment
+  int64_t q_start;  // first query token of the segment (row of q and o)
+  int64_t k_start;  // first key token of the segment (row of k and v)
+  int q_len;        // queries of the segment
+  int k_len;        // keys of the segment
+  int h;            // head
+  int q_begin;      // first query of the tile, relative to the segment
+  int tile_begin;   // first key tile of the item
+  int ntiles;       // key tiles of the item
 };
+
+// Where the results of an item go.  kFinal: O as bf16 [Tq][H][D] and, when lse is not null,
+// the natural log-sum-exp of every row as float [Tq][H].  kPartial (one key range of a split
+// call): the normalised O of that range as float [splits][Tq][H][D] and its log-sum-exp as
+// float [splits][Tq][H], combined afterwards by attn_merge_kernel.
+enum OutMode { kFinal = 0, kPartial = 1 };
+struct Out {
+  __bf16* o;
+  float* lse;
+  float* part_o;
+  float* part_lse;
+  int64_t tq;  // query rows of the whole call (one split's slab is tq x H rows)
+  int split;   // key range of this item (kPartial)
+};
+
+constexpr float kLn2 = 0.6931471805599453f;
 
 // XCD-aware order: workgroup b runs on XCD b % 8; consecutive workgroups of one XCD take
 // `chunk` consecutive items, and every 8*chunk workgroups cover 8*chunk consecutive items,
@@ -398,10 +421,15 @@ __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const ld
 // Fetches past the segment end read zeros and land in stages nobody reads any more, so the
 // schedule has no branches.  The two groups are separate instantiations, so each has a
 // straight-line schedule.
-template <int D, bool kGroupB>
+template <int D, int kMode>
+__device__ __forceinline__ void write_result(const Item& it, const Out& out,
+                                             const f32x16 (&oacc)[D / 32], float l_tot, float m_c,
+                                             int H, int qrow, int hb);
+
+template <int D, bool kGroupB, int kMode>
 __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __restrict__ q,
                                                const __bf16* __restrict__ k,
-                                               const __bf16* __restrict__ v, __bf16* __restrict__ o,
+                                               const __bf16* __restrict__ v, const Out& out,
                                                int H, float c, bool negate_q, char* smem) {
   using G = Geo<D>;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -409,11 +437,14 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   const int gw = wave & (G::kGroupWaves - 1);  // wave inside its group
   const int hb = lane >> 5, col = lane & 31;
   const int row_bytes = H * D * 2;
-  const int64_t base = (it.seg_start * H + it.h) * D;  // element offset of (first token, h)
-  const uint32_t seg_bytes = (uint32_t)(it.seg_len - 1) * (uint32_t)row_bytes + D * 2;
-  __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, seg_bytes);
-  __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, seg_bytes);
-  __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, seg_bytes);
+  // element offsets of (first query, h) and (first key, h); byte ranges of the segment's rows
+  const int64_t qbase = (it.q_start * H + it.h) * D;
+  const int64_t kbase = (it.k_start * H + it.h) * D;
+  const uint32_t q_bytes = (uint32_t)(it.q_len - 1) * (uint32_t)row_bytes + D * 2;
+  const uint32_t k_bytes = (uint32_t)(it.k_len - 1) * (uint32_t)row_bytes + D * 2;
+  __amdgpu_buffer_rsrc_t rq = make_rsrc(q + qbase, q_bytes);
+  __amdgpu_buffer_rsrc_t rk = make_rsrc(k + kbase, k_bytes);
+  __amdgpu_buffer_rsrc_t rv = make_rsrc(v + kbase, k_bytes);
   lds_char* const lds = (lds_char*)smem;
   auto ktile = [&](int stage) { return lds + G::kKRing + stage * G::kKTile; };
   auto vtile = [&](int stage) { return lds + G::kVRing + stage * G::kVTile; };
@@ -421,10 +452,11 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   int koff[G::kKDmaMax], voff[G::kVDmaPerWave];
   if (!kGroupB) dma_offsets_k<D>(gw, lane, row_bytes, koff);
   else dma_offsets_v<D>(gw, lane, row_bytes, voff);
-  // this group's fetch of tile j (K for group A, V for group B) into stage j % 3
+  // this group's fetch of the item's tile j (K for group A, V for group B) into stage j % 3
   auto fetch = [&](int j, int stage) {
-    if (!kGroupB) dma_k<D>(rk, j * kBN, row_bytes, ktile(stage), koff, gw);
-    else dma_v<D>(rv, j * kBN, row_bytes, vtile(stage), voff, gw);
+    const int key0 = (it.tile_begin + j) * kBN;
+    if (!kGroupB) dma_k<D>(rk, key0, row_bytes, ktile(stage), koff, gw);
+    else dma_v<D>(rv, key0, row_bytes, vtile(stage), voff, gw);
   };
   constexpr int kFetchWait = kGroupB ? G::kVDmaPerWave : G::kKDmaMin;  // fewest per wave
 
@@ -446,8 +478,9 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   float m_c = -INFINITY, l_part = 0.0f, alpha = 1.0f;
   bool rescale = false;
 
-  const int ntiles = (it.seg_len + kBN - 1) / kBN;
-  const int last_keys = it.seg_len - (ntiles - 1) * kBN;  // valid keys of the last tile
+  const int ntiles = it.ntiles;
+  // valid keys of the item's last tile: fewer than kBN only on the segment's ragged last tile
+  const int last_keys = min(kBN, it.k_len - (it.tile_begin + ntiles - 1) * kBN);
   // vector step j: fetch tile j + 2 into stage st2, softmax S_j -> P_j, wait for the fetch of
   // the previous vector step, barrier; kMasked on the ragged last tile only
   auto vstep = [&](int j, int st2, auto masked) {
@@ -501,32 +534,78 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
   wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
 
-  // ---- epilogue: O = O / l, bf16; rows past the segment end are dropped by the range check
-  __amdgpu_buffer_rsrc_t ro = make_rsrc(o + base, seg_bytes);
-  const float l_tot = half_sum(l_part);
-  const float inv = 1.0f / l_tot;
-#pragma unroll
-  for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      f32x4 x = {oacc[db][4 * g4] * inv, oacc[db][4 * g4 + 1] * inv, oacc[db][4 * g4 + 2] * inv,
-                 oacc[db][4 * g4 + 3] * inv};
-      bf16x4 b = __builtin_convertvector(x, bf16x4);
-      u32x2 w = __builtin_bit_cast(u32x2, b);
-      const int ch = 32 * db + 8 * g4 + 4 * hb;  // first of 4 channels
-      __builtin_amdgcn_raw_buffer_store_b64(w, ro, qrow * row_bytes + ch * 2, 0, 0);
-    }
+  write_result<D, kMode>(it, out, oacc, half_sum(l_part), m_c, H, qrow, hb);
 }
 
-template <int D>
+// The epilogue of one wave: O = O / l for its 32 query rows, and the row's natural log-sum-exp
+// lse = (m_c + log2 l) ln 2 (m_c is in log2 units of the scaled scores).  l_tot = 0 marks an
+// item without keys: O = 0 and lse = -inf.  Rows past the segment end are dropped by the
+// descriptors' range checks.
+template <int D, int kMode>
+__device__ __forceinline__ void write_result(const Item& it, const Out& out,
+                                             const f32x16 (&oacc)[D / 32], float l_tot, float m_c,
+                                             int H, int qrow, int hb) {
+  const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+  const float lse = l_tot > 0.0f ? (m_c + log2f(l_tot)) * kLn2 : -INFINITY;
+  const uint32_t lse_bytes = ((uint32_t)(it.q_len - 1) * (uint32_t)H + 1) * 4;
+  if (kMode == kFinal) {
+    const int row_bytes = H * D * 2;
+    const uint32_t q_bytes = (uint32_t)(it.q_len - 1) * (uint32_t)row_bytes + D * 2;
+    __amdgpu_buffer_rsrc_t ro = make_rsrc(out.o + (it.q_start * H + it.h) * D, q_bytes);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        f32x4 x = {oacc[db][4 * g4] * inv, oacc[db][4 * g4 + 1] * inv, oacc[db][4 * g4 + 2] * inv,
+                   oacc[db][4 * g4 + 3] * inv};
+        bf16x4 b = __builtin_convertvector(x, bf16x4);
+        u32x2 w = __builtin_bit_cast(u32x2, b);
+        const int ch = 32 * db + 8 * g4 + 4 * hb;  // first of 4 channels
+        __builtin_amdgcn_raw_buffer_store_b64(w, ro, qrow * row_bytes + ch * 2, 0, 0);
+      }
+    if (out.lse != nullptr && hb == 0) {
+      __amdgpu_buffer_rsrc_t rl = make_rsrc(out.lse + it.q_start * H + it.h, lse_bytes);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, qrow * H * 4, 0, 0);
+    }
+  } else {
+    const int64_t slab = (int64_t)out.split * out.tq;  // first row of this split's slab
+    const uint32_t o_bytes = ((uint32_t)(it.q_len - 1) * (uint32_t)H + 1) * D * 4;
+    __amdgpu_buffer_rsrc_t rpo = make_rsrc(out.part_o + ((slab + it.q_start) * H + it.h) * D, o_bytes);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        f32x4 x = {oacc[db][4 * g4] * inv, oacc[db][4 * g4 + 1] * inv, oacc[db][4 * g4 + 2] * inv,
+                   oacc[db][4 * g4 + 3] * inv};
+        const int ch = 32 * db + 8 * g4 + 4 * hb;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), rpo,
+                                               (qrow * H * D + ch) * 4, 0, 0);
+      }
+    if (hb == 0) {
+      __amdgpu_buffer_rsrc_t rl = make_rsrc(out.part_lse + (slab + it.q_start) * H + it.h, lse_bytes);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, qrow * H * 4, 0, 0);
+    }
+  }
+}
+
+template <int D, int kMode>
 __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
                                          const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-                                         __bf16* __restrict__ o, int H, float c, bool negate_q,
-                                         char* smem) {
-  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= kWaves / 2)
-    run_item_group<D, true>(it, q, k, v, o, H, c, negate_q, smem);
+                                         const Out& out, int H, float c, bool negate_q, char* smem) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (it.ntiles <= 0) {  // no keys in this item (the whole workgroup leaves together)
+    const int lane = threadIdx.x & 63;
+    f32x16 zero[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) zero[db] = f32x16{};
+    write_result<D, kMode>(it, out, zero, 0.0f, -INFINITY, H, it.q_begin + 32 * wave + (lane & 31),
+                           lane >> 5);
+    return;
+  }
+  if (wave >= kWaves / 2)
+    run_item_group<D, true, kMode>(it, q, k, v, out, H, c, negate_q, smem);
   else
-    run_item_group<D, false>(it, q, k, v, o, H, c, negate_q, smem);
+    run_item_group<D, false, kMode>(it, q, k, v, out, H, c, negate_q, smem);
 }
 
 template <int D>
@@ -538,21 +617,28 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
   const int item = remap_block(blockIdx.x, total, chunk);
   const int bh = item / nq;
   Item it;
-  it.seg_len = L;
-  it.seg_start = (int64_t)(bh / H) * L;
+  it.q_start = it.k_start = (int64_t)(bh / H) * L;
+  it.q_len = it.k_len = L;
   it.h = bh % H;
   it.q_begin = (item % nq) * kBM;
-  run_item<D>(it, q, k, v, o, H, c, negate_q != 0, smem);
+  it.tile_begin = 0;
+  it.ntiles = (L + kBN - 1) / kBN;
+  Out out{o, nullptr, nullptr, nullptr, 0, 0};
+  run_item<D, kFinal>(it, q, k, v, out, H, c, negate_q != 0, smem);
 }
 
-// plan layout (int32): [0] item count, [1] error flag, then per rank r (longest segment
-// first): [2 + 2r] segment index, [3 + 2r] first item of that segment.
-template <int D>
+// Packed batch: segment s has queries [cu_q[s], cu_q[s+1]) and keys [cu_k[s], cu_k[s+1])
+// (cu_k == cu_q for self-attention).  Each (segment, head, query tile) is split into n_split
+// items over consecutive ranges of the segment's key tiles (n_split = 1: one item, kFinal).
+// plan layout (int32): [0] item count, [1] error flag, then per rank r (most keys first):
+// [2 + 2r] segment index, [3 + 2r] first item of that segment.  The items of a segment are
+// ordered head-major, then split, then query tile, so consecutive items share K/V ranges.
+template <int D, int kMode>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
-                   const __bf16* __restrict__ v, __bf16* __restrict__ o,
-                   const int32_t* __restrict__ cu, const int32_t* __restrict__ plan, int nseq,
-                   int H, int chunk, float c, int negate_q) {
+                   const __bf16* __restrict__ v, Out out, const int32_t* __restrict__ cu_q,
+                   const int32_t* __restrict__ cu_k, const int32_t* __restrict__ plan, int nseq,
+                   int H, int n_split, int chunk, float c, int negate_q) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int total = plan[0];
   if ((int)blockIdx.x >= total) return;
@@ -566,29 +652,77 @@ attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
   const int s = plan[2 + 2 * lo];
   const int local = item - plan[3 + 2 * lo];
   Item it;
-  it.seg_start = cu[s];
-  it.seg_len = cu[s + 1] - cu[s];
-  const int nq = (it.seg_len + kBM - 1) / kBM;
-  it.h = local / nq;
+  it.q_start = cu_q[s];
+  it.q_len = cu_q[s + 1] - cu_q[s];
+  it.k_start = cu_k[s];
+  it.k_len = cu_k[s + 1] - cu_k[s];
+  const int nq = (it.q_len + kBM - 1) / kBM;
+  const int per_head = nq * n_split;
+  it.h = local / per_head;
+  const int split = (local % per_head) / nq;
   it.q_begin = (local % nq) * kBM;
-  run_item<D>(it, q, k, v, o, H, c, negate_q != 0, smem);
+  const int seg_tiles = (it.k_len + kBN - 1) / kBN;
+  const int per_split = (seg_tiles + n_split - 1) / n_split;
+  it.tile_begin = split * per_split;
+  it.ntiles = max(0, min(per_split, seg_tiles - it.tile_begin));
+  out.split = split;
+  run_item<D, kMode>(it, q, k, v, out, H, c, negate_q != 0, smem);
 }
 
-// ---- planning kernel: validate cu_seqlens, order segments longest first, prefix-sum items.
+// Combines the key ranges of a split call: for every (query row, head) with partial results
+// (O_i, lse_i) over disjoint key ranges, O = sum_i exp(lse_i - lse) O_i with
+// lse = log sum_i exp(lse_i) -- a softmax-weighted average over the union of the ranges.  One
+// thread per 8 channels of a row; rows = Tq * H.
+constexpr int kMergeThreads = 256;
+
+template <int D>
+__global__ void __launch_bounds__(kMergeThreads)
+attn_merge_kernel(const float* __restrict__ part_o, const float* __restrict__ part_lse,
+                  int n_split, int64_t rows, __bf16* __restrict__ o, float* __restrict__ lse) {
+  constexpr int kChunks = D / 8;
+  const int64_t gid = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
+  const int64_t row = gid / kChunks;
+  const int c8 = (int)(gid % kChunks);
+  if (row >= rows) return;
+  float m = -INFINITY;
+  for (int i = 0; i < n_split; ++i) m = fmaxf(m, part_lse[i * rows + row]);
+  f32x4 a0 = {0.0f, 0.0f, 0.0f, 0.0f}, a1 = a0;
+  float wsum = 0.0f;
+  if (m != -INFINITY) {
+    for (int i = 0; i < n_split; ++i) {
+      const float w = expf(part_lse[i * rows + row] - m);  // 0 for a range without keys
+      const f32x4* src = (const f32x4*)(part_o + (i * rows + row) * D + c8 * 8);
+      a0 += w * src[0];
+      a1 += w * src[1];
+      wsum += w;
+    }
+  }
+  const float inv = wsum > 0.0f ? 1.0f / wsum : 0.0f;
+  f32x4 r0 = a0 * inv, r1 = a1 * inv;
+  bf16x4 b0 = __builtin_convertvector(r0, bf16x4), b1 = __builtin_convertvector(r1, bf16x4);
+  bf16x8 b = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+  *(bf16x8*)(o + row * D + c8 * 8) = b;
+  if (lse != nullptr && c8 == 0) lse[row] = wsum > 0.0f ? m + logf(wsum) : -INFINITY;
+}
+
+// ---- planning kernel: validate the offsets, order segments by key count (the cost of each of
+// their items) longest first, prefix-sum the items.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanSortMax = 4096;  // larger batches keep their given order
 
 __global__ void __launch_bounds__(kPlanThreads)
-plan_kernel(const int32_t* __restrict__ cu, int nseq, int max_seqlen, int total_tokens, int H,
+plan_kernel(const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int nseq,
+            int max_q, int max_k, int total_q, int total_k, int H, int n_split,
             int32_t* __restrict__ plan) {
   __shared__ uint64_t keys[kPlanSortMax];
   __shared__ int32_t scan[kPlanThreads];
   const int tid = threadIdx.x;
   int bad = 0;
-  if (tid == 0 && (cu[0] != 0 || cu[nseq] != total_tokens)) bad = 1;
+  if (tid == 0 && (cu_q[0] != 0 || cu_q[nseq] != total_q || cu_k[0] != 0 || cu_k[nseq] != total_k))
+    bad = 1;
   for (int s = tid; s < nseq; s += kPlanThreads) {
-    int len = cu[s + 1] - cu[s];
-    if (len < 0 || len > max_seqlen) bad = 1;
+    const int lq = cu_q[s + 1] - cu_q[s], lk = cu_k[s + 1] - cu_k[s];
+    if (lq < 0 || lq > max_q || lk < 0 || lk > max_k) bad = 1;
   }
   if (__syncthreads_or(bad)) {
     if (tid == 0) { plan[0] = 0; plan[1] = 1; }
@@ -598,10 +732,10 @@ plan_kernel(const int32_t* __restrict__ cu, int nseq, int max_seqlen, int total_
   if (sorted) {
     int n2 = 1;
     while (n2 < nseq) n2 <<= 1;
-    // key: (max - length) in the high word, index in the low word -> ascending = longest first
+    // key: (max - keys) in the high word, index in the low word -> ascending = most keys first
     for (int i = tid; i < n2; i += kPlanThreads) {
       if (i < nseq) {
-        uint32_t len = (uint32_t)(cu[i + 1] - cu[i]);
+        uint32_t len = (uint32_t)(cu_k[i + 1] - cu_k[i]);
         keys[i] = ((uint64_t)(0x7fffffffu - len) << 32) | (uint32_t)i;
       } else {
         keys[i] = ~0ull;
@@ -621,15 +755,15 @@ plan_kernel(const int32_t* __restrict__ cu, int nseq, int max_seqlen, int total_
         __syncthreads();
       }
   }
-  // exclusive prefix sum of H * ceil(len / kBM) in rank order, 1024 ranks per pass
+  // exclusive prefix sum of H * n_split * ceil(queries / kBM) in rank order, 1024 ranks per pass
   int carry = 0;
   for (int base = 0; base < nseq; base += kPlanThreads) {
     int r = base + tid;
     int seg = 0, cnt = 0;
     if (r < nseq) {
       seg = sorted ? (int)(keys[r] & 0xffffffffu) : r;
-      int len = cu[seg + 1] - cu[seg];
-      cnt = H * ((len + kBM - 1) / kBM);
+      const int lq = cu_q[seg + 1] - cu_q[seg];
+      cnt = H * n_split * ((lq + kBM - 1) / kBM);
     }
     scan[tid] = cnt;
     __syncthreads();
@@ -664,23 +798,42 @@ static hipError_t launch_dense_d(const DenseArgs& a, hipStream_t st) {
 }
 
 template <int D>
-static hipError_t launch_varlen_d(const VarlenArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a.cu_seqlens, a.nseq,
-                     a.max_seqlen, a.total_tokens, a.H, a.plan);
+static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a.cu_q, a.cu_k, a.nseq,
+                     a.max_q, a.max_k, a.total_q, a.total_k, a.H, a.n_split, a.plan);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t grid = varlen_grid_bound(a.total_tokens, a.nseq, a.H);
+  const int64_t grid = packed_grid_bound(a.total_q, a.nseq, a.H, a.n_split);
   const float c = fabsf(a.scale) * kLog2e;
-  hipLaunchKernelGGL((attn_varlen_kernel<D>), dim3((unsigned)grid), dim3(kThreads), Geo<D>::kLds,
-                     st, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (__bf16*)a.o, a.cu_seqlens, a.plan, a.nseq, a.H, a.xcd_chunk, c,
-                     a.scale < 0.0f ? 1 : 0);
+  const int neg = a.scale < 0.0f ? 1 : 0;
+  Out out{(__bf16*)a.o, a.lse, a.part_o, a.part_lse, a.total_q, 0};
+  if (a.n_split == 1) {
+    hipLaunchKernelGGL((attn_varlen_kernel<D, kFinal>), dim3((unsigned)grid), dim3(kThreads),
+                       Geo<D>::kLds, st, (const __bf16*)a.q, (const __bf16*)a.k,
+                       (const __bf16*)a.v, out, a.cu_q, a.cu_k, a.plan, a.nseq, a.H, 1,
+                       a.xcd_chunk, c, neg);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((attn_varlen_kernel<D, kPartial>), dim3((unsigned)grid), dim3(kThreads),
+                     Geo<D>::kLds, st, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
+                     out, a.cu_q, a.cu_k, a.plan, a.nseq, a.H, a.n_split, a.xcd_chunk, c, neg);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t rows = (int64_t)a.total_q * a.H;
+  const int64_t threads = rows * (D / 8);
+  const int64_t blocks = (threads + kMergeThreads - 1) / kMergeThreads;
+  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
+                     a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse);
   return hipGetLastError();
 }
 
-int64_t varlen_grid_bound(int32_t total_tokens, int32_t nseq, int32_t H) {
-  // sum_s ceil(L_s / BM) <= ceil(T / BM) + nseq
-  return (int64_t)H * (((int64_t)total_tokens + kBM - 1) / kBM + nseq);
+int64_t packed_grid_bound(int32_t total_q, int32_t nseq, int32_t H, int32_t n_split) {
+  // sum_s ceil(Lq_s / BM) <= ceil(Tq / BM) + nseq
+  return (int64_t)H * n_split * (((int64_t)total_q + kBM - 1) / kBM + nseq);
+}
+
+int64_t merge_blocks(int32_t total_q, int32_t H, int32_t d) {
+  return ((int64_t)total_q * H * (d / 8) + kMergeThreads - 1) / kMergeThreads;
 }
 
 int64_t plan_ints(int32_t nseq) { return 2 + 2 * (int64_t)nseq; }
@@ -695,19 +848,24 @@ hipError_t configure_kernels() {
   e = hipFuncSetAttribute((const void*)attn_dense_kernel<128>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, Geo<128>::kLds);
   if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)attn_varlen_kernel<64>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<64>::kLds);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)attn_varlen_kernel<128>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize, Geo<128>::kLds);
+  const void* packed[4] = {(const void*)attn_varlen_kernel<64, kFinal>,
+                           (const void*)attn_varlen_kernel<64, kPartial>,
+                           (const void*)attn_varlen_kernel<128, kFinal>,
+                           (const void*)attn_varlen_kernel<128, kPartial>};
+  for (int i = 0; i < 4; ++i) {
+    e = hipFuncSetAttribute(packed[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                            i < 2 ? Geo<64>::kLds : Geo<128>::kLds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_dense(const DenseArgs& a, hipStream_t st) {
   return a.d == 64 ? launch_dense_d<64>(a, st) : launch_dense_d<128>(a, st);
 }
 
-hipError_t launch_varlen(const VarlenArgs& a, hipStream_t st) {
-  return a.d == 64 ? launch_varlen_d<64>(a, st) : launch_varlen_d<128>(a, st);
+hipError_t launch_packed(const PackedArgs& a, hipStream_t st) {
+  return a.d == 64 ? launch_packed_d<64>(a, st) : launch_packed_d<128>(a, st);
 }
 
 }  // namespace tsattn

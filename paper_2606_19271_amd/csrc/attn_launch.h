@@ -16,20 +16,30 @@ struct DenseArgs {
   int xcd_chunk;  // consecutive items per XCD (CUs per XCD x workgroups per CU)
 };
 
-struct VarlenArgs {
+// A packed batch: segment s has queries [cu_q[s], cu_q[s+1]) of q/o and keys/values
+// [cu_k[s], cu_k[s+1]) of k/v (cu_k == cu_q for self-attention).  With n_split > 1 every
+// (segment, head, query tile) is split over n_split key ranges whose partial results go to
+// part_o / part_lse and are merged into o (and lse) by a second kernel.
+struct PackedArgs {
   const void* q;
   const void* k;
   const void* v;
   void* o;
-  const int32_t* cu_seqlens;  // device
-  int32_t nseq, max_seqlen, total_tokens, H, d;
+  float* lse;            // device [total_q][H] or null
+  const int32_t* cu_q;   // device
+  const int32_t* cu_k;   // device
+  int32_t nseq, max_q, max_k, total_q, total_k, H, d, n_split;
   float scale;
   int xcd_chunk;
-  int32_t* plan;  // device, plan_ints(nseq) entries
+  int32_t* plan;         // device, plan_ints(nseq) entries
+  float* part_o;         // device [n_split][total_q][H][d] (n_split > 1)
+  float* part_lse;       // device [n_split][total_q][H] (n_split > 1)
 };
 
 // Upper bound of the number of work items of a packed batch (its launch grid).
-int64_t varlen_grid_bound(int32_t total_tokens, int32_t nseq, int32_t H);
+int64_t packed_grid_bound(int32_t total_q, int32_t nseq, int32_t H, int32_t n_split);
+// Workgroups of the merge kernel of a split call.
+int64_t merge_blocks(int32_t total_q, int32_t H, int32_t d);
 // int32 entries of the plan buffer for nseq segments.
 int64_t plan_ints(int32_t nseq);
 // Queries per work item.
@@ -37,6 +47,6 @@ int query_tile();
 
 hipError_t configure_kernels();
 hipError_t launch_dense(const DenseArgs& a, hipStream_t st);
-hipError_t launch_varlen(const VarlenArgs& a, hipStream_t st);
+hipError_t launch_packed(const PackedArgs& a, hipStream_t st);
 
 }  // namespace tsattn

@@ -17,11 +17,13 @@ namespace {
 constexpr int kMaxDevices = 64;
 constexpr int64_t kByteLimit = (int64_t)1 << 31;
 constexpr int64_t kGridLimit = (int64_t)1 << 23;  // workgroups per launch (x 512 threads < 2^32)
+constexpr int32_t kMaxSplits = 16;                 // key ranges per query tile of a split call
 
 struct DeviceState {
   std::once_flag once;
   int status = TS_ERR_UNSUPPORTED;  // TS_OK once the device is known to be usable
   int xcd_chunk = 32;
+  int cus = 256;
   hipMemPool_t pool = nullptr;
 };
 
@@ -33,6 +35,7 @@ void init_device(int dev, DeviceState* st) {
   if (strncmp(p.gcnArchName, "gfx950", 6) != 0) { st->status = TS_ERR_UNSUPPORTED; return; }
   // gfx950: 8 XCDs; one 512-thread workgroup resides per CU.
   st->xcd_chunk = p.multiProcessorCount / 8 > 0 ? p.multiProcessorCount / 8 : 1;
+  st->cus = p.multiProcessorCount;
   if (tsattn::configure_kernels() != hipSuccess) { st->status = TS_ERR_HIP; return; }
   hipMemPoolProps props;
   memset(&props, 0, sizeof props);
@@ -68,6 +71,12 @@ bool overlaps(const void* a, const void* b, int64_t bytes) {
   return x < y + (uintptr_t)bytes && y < x + (uintptr_t)bytes;
 }
 
+// [a, a + na) and [b, b + nb) share a byte (empty ranges share none).
+bool ranges_overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+  uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
 // Shared checks of both entry points; tokens = rows of q/k/v/o, longest = longest segment.
 int check_common(const void* q, const void* k, const void* v, const void* o, int64_t tokens,
                  int64_t longest, int32_t H, int32_t d, float scale) {
@@ -87,6 +96,78 @@ int check_common(const void* q, const void* k, const void* v, const void* o, int
 bool validate_mode() {
   const char* e = getenv("TS_ATTN_VALIDATE");
   return e && e[0] == '1';
+}
+
+// Checks of the chunk-vs-cache call: q/o hold tq rows, k/v tk rows; segments are at most
+// max_q queries and max_k keys long.
+int check_kv(const void* q, const void* k, const void* v, const void* o, const float* lse,
+             int64_t tq, int64_t tk, int64_t max_q, int64_t max_k, int32_t H, int32_t d,
+             float scale) {
+  if (!q || !k || !v || !o) return TS_ERR_NULL;
+  if (H < 1 || tq < 0 || tk < 0 || max_q < 0 || max_k < 0) return TS_ERR_SHAPE;
+  if (d != 64 && d != 128) return TS_ERR_HEAD_DIM;
+  if (!isfinite(scale)) return TS_ERR_SCALE;
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return TS_ERR_ALIGN;
+  if (((uintptr_t)lse & 3u) != 0) return TS_ERR_ALIGN;
+  const int64_t row_bytes = (int64_t)H * d * 2;
+  if ((max_q + 256) * row_bytes >= kByteLimit || (max_k + 256) * row_bytes >= kByteLimit)
+    return TS_ERR_SHAPE;
+  if (tq > (int64_t)1 << 31 || tk > (int64_t)1 << 31) return TS_ERR_SHAPE;
+  const int64_t qb = tq * row_bytes, kb = tk * row_bytes;
+  if (ranges_overlap(o, qb, q, qb) || ranges_overlap(o, qb, k, kb) || ranges_overlap(o, qb, v, kb))
+    return TS_ERR_ALIAS;
+  if (lse) {
+    const int64_t lb = tq * H * 4;
+    if (ranges_overlap(lse, lb, q, qb) || ranges_overlap(lse, lb, k, kb) ||
+        ranges_overlap(lse, lb, v, kb) || ranges_overlap(lse, lb, o, qb))
+      return TS_ERR_ALIAS;
+  }
+  return TS_OK;
+}
+
+// Key ranges per query tile when the caller leaves the choice to the library: enough work
+// items for about two workgroups per CU, with at least 8 key tiles (512 keys) per range.
+int32_t auto_splits(int cus, int32_t total_q, int32_t max_k, int32_t H) {
+  const int64_t items = (int64_t)H * ((total_q + 255) / 256);
+  const int64_t target = 2 * (int64_t)cus;
+  if (items <= 0 || items >= target) return 1;
+  int64_t n = (target + items - 1) / items;
+  const int64_t cap = ((int64_t)max_k + 511) / 512;
+  if (n > cap) n = cap;
+  if (n > kMaxSplits) n = kMaxSplits;
+  return n < 1 ? 1 : (int32_t)n;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Plan buffer (and split workspace) from the device's pool, the launches, the optional
+// validation read-back, and the stream-ordered release.
+int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
+  const size_t plan_bytes = align256((size_t)tsattn::plan_ints(a.nseq) * sizeof(int32_t));
+  size_t bytes = plan_bytes;
+  size_t lse_bytes = 0;
+  if (a.n_split > 1) {
+    lse_bytes = align256((size_t)a.n_split * a.total_q * a.H * sizeof(float));
+    bytes += lse_bytes + (size_t)a.n_split * a.total_q * a.H * a.d * sizeof(float);
+  }
+  char* buf = nullptr;
+  if (hipMallocFromPoolAsync((void**)&buf, bytes, st->pool, s) != hipSuccess) return TS_ERR_NOMEM;
+  a.plan = (int32_t*)buf;
+  if (a.n_split > 1) {
+    a.part_lse = (float*)(buf + plan_bytes);
+    a.part_o = (float*)(buf + plan_bytes + lse_bytes);
+  }
+  int rc = tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
+  if (rc == TS_OK && validate_mode()) {
+    int32_t head[2] = {0, 0};
+    if (hipMemcpyAsync(head, a.plan, sizeof head, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      rc = TS_ERR_HIP;
+    else if (head[1] != 0)
+      rc = TS_ERR_SEGMENTS;
+  }
+  if (hipFreeAsync(buf, s) != hipSuccess && rc == TS_OK) rc = TS_ERR_HIP;
+  return rc;
 }
 
 }  // namespace
@@ -132,28 +213,35 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
   if (nseq < 0 || max_seqlen < 0 || total_tokens < 0) return TS_ERR_SHAPE;
   int rc = check_common(q, k, v, o, total_tokens, max_seqlen, H, d, scale);
   if (rc != TS_OK) return rc;
-  if (tsattn::varlen_grid_bound(total_tokens, nseq, H) >= kGridLimit) return TS_ERR_SHAPE;
+  if (tsattn::packed_grid_bound(total_tokens, nseq, H, 1) >= kGridLimit) return TS_ERR_SHAPE;
   if (nseq == 0 || total_tokens == 0) return TS_OK;
   DeviceState* st = current_device(&rc);
   if (!st) return rc;
-  hipStream_t s = (hipStream_t)stream;
-  int32_t* plan = nullptr;
-  const size_t plan_bytes = (size_t)tsattn::plan_ints(nseq) * sizeof(int32_t);
-  if (hipMallocFromPoolAsync((void**)&plan, plan_bytes, st->pool, s) != hipSuccess)
-    return TS_ERR_NOMEM;
-  tsattn::VarlenArgs a{q, k, v, o, cu_seqlens, nseq, max_seqlen, total_tokens, H, d, scale,
-                       st->xcd_chunk, plan};
-  rc = tsattn::launch_varlen(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
-  if (rc == TS_OK && validate_mode()) {
-    int32_t head[2] = {0, 0};
-    if (hipMemcpyAsync(head, plan, sizeof head, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
-      rc = TS_ERR_HIP;
-    else if (head[1] != 0)
-      rc = TS_ERR_SEGMENTS;
-  }
-  if (hipFreeAsync(plan, s) != hipSuccess && rc == TS_OK) rc = TS_ERR_HIP;
-  return rc;
+  tsattn::PackedArgs a{q, k, v, o, nullptr, cu_seqlens, cu_seqlens, nseq, max_seqlen, max_seqlen,
+                       total_tokens, total_tokens, H, d, 1, scale, st->xcd_chunk,
+                       nullptr, nullptr, nullptr};
+  return run_packed(st, a, (hipStream_t)stream);
+}
+
+int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, float* lse,
+                        const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int32_t nseq,
+                        int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
+                        int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits,
+                        void* stream) {
+  if (!cu_seqlens_q || !cu_seqlens_k) return TS_ERR_NULL;
+  if (nseq < 0 || num_splits < 0 || num_splits > kMaxSplits) return TS_ERR_SHAPE;
+  int rc = check_kv(q, k, v, o, lse, total_q, total_k, max_seqlen_q, max_seqlen_k, H, d, scale);
+  if (rc != TS_OK) return rc;
+  if (tsattn::packed_grid_bound(total_q, nseq, H, kMaxSplits) >= kGridLimit) return TS_ERR_SHAPE;
+  if (tsattn::merge_blocks(total_q, H, d) >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
+  if (nseq == 0 || total_q == 0) return TS_OK;
+  DeviceState* st = current_device(&rc);
+  if (!st) return rc;
+  const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H);
+  tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
+                       max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
+                       nullptr, nullptr, nullptr};
+  return run_packed(st, a, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -33,8 +33,8 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert names == ["ts_attn_abi_version", "ts_attn_fwd", "ts_attn_fwd_varlen",
-                     "ts_attn_status_str"]
+    assert names == ["ts_attn_abi_version", "ts_attn_fwd", "ts_attn_fwd_kvcache",
+                     "ts_attn_fwd_varlen", "ts_attn_status_str"]
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB], capture_output=True, text=True,
@@ -112,6 +112,36 @@ def test_varlen_argument_checks(lib):
     assert varlen(lib, T=0) == _lib.TS_OK
 
 
+def kvcache(lib, q=A, k=A, v=A, o=BIG, lse=None, cuq=A, cuk=A, nseq=2, max_q=64, max_k=256,
+            tq=128, tk=512, H=2, d=128, scale=0.125, splits=0):
+    P = ctypes.c_void_p
+    return lib.ts_attn_fwd_kvcache(P(q), P(k), P(v), P(o), P(lse), P(cuq), P(cuk), nseq, max_q,
+                                   max_k, tq, tk, H, d, scale, splits, P(None))
+
+
+def test_kvcache_argument_checks(lib):
+    assert kvcache(lib, cuk=0) == _lib.TS_ERR_NULL
+    assert kvcache(lib, cuq=0) == _lib.TS_ERR_NULL
+    assert kvcache(lib, v=0) == _lib.TS_ERR_NULL
+    assert kvcache(lib, nseq=-1) == _lib.TS_ERR_SHAPE
+    assert kvcache(lib, max_k=-1) == _lib.TS_ERR_SHAPE
+    assert kvcache(lib, tk=-1) == _lib.TS_ERR_SHAPE
+    assert kvcache(lib, splits=-1) == _lib.TS_ERR_SHAPE
+    assert kvcache(lib, splits=17) == _lib.TS_ERR_SHAPE
+    assert kvcache(lib, d=96) == _lib.TS_ERR_HEAD_DIM
+    assert kvcache(lib, scale=math.inf) == _lib.TS_ERR_SCALE
+    assert kvcache(lib, k=A + 8) == _lib.TS_ERR_ALIGN
+    assert kvcache(lib, lse=BIG * 2 + 2) == _lib.TS_ERR_ALIGN
+    # o holds tq rows; k/v hold tk rows: o placed inside k's range aliases
+    row = 2 * 128 * 2
+    assert kvcache(lib, o=A + 300 * row) == _lib.TS_ERR_ALIAS       # inside k/v (512 rows)
+    assert kvcache(lib, lse=BIG + 64) == _lib.TS_ERR_ALIAS          # lse inside o
+    assert kvcache(lib, max_k=300000, H=40) == _lib.TS_ERR_SHAPE    # beyond the byte limit
+    # empty problems are no-ops that never touch the device
+    assert kvcache(lib, nseq=0) == _lib.TS_OK
+    assert kvcache(lib, tq=0) == _lib.TS_OK
+
+
 def test_python_binding_rejects_cpu_tensors():
     import torch
     x = torch.zeros((1, 8, 1, 64), dtype=torch.bfloat16)
@@ -119,3 +149,7 @@ def test_python_binding_rejects_cpu_tensors():
         ts.ts_attn_fwd(x, x, x)
     with pytest.raises(ValueError):
         ts.ts_attn_fwd_varlen(x[0], x[0], x[0], torch.tensor([0, 8], dtype=torch.int32), 8)
+
+    with pytest.raises(ValueError):
+        cu = torch.tensor([0, 8], dtype=torch.int32)
+        ts.ts_attn_fwd_kvcache(x[0], x[0], x[0], cu, cu, 8, 8)

@@ -1,0 +1,178 @@
+"""GPU parity of ts_attn_fwd_kvcache (chunk queries against per-session key/value ranges, with the
+log-sum-exp output and the split-key path) against the fp64 oracle, through the C ABI.
+
+Bars: the output O to the same bar as every other entry point (tests/metrics.py).  The lse to an
+absolute 1e-2: the kernel's lse is (running max + log2 of the fp32 sum of the bf16-rounded
+weights) * ln 2, and rounding each weight to bf16 changes that sum by at most 2^-9 relative,
+i.e. the lse by at most 2e-3 (plus fp32 rounding); the bar leaves a factor of five.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from metrics import assert_parity
+from oracle import ts_ref
+
+pytestmark = pytest.mark.gpu
+
+ts = pytest.importorskip("paper_2606_19271_amd")
+
+LSE_ABS = 1e-2
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ts.load()
+    return torch.device("cuda:0")
+
+
+def draw(lq, lk, H, d, seed, k_offset=False):
+    w = W.KvWorkload("custom", tuple(lq), tuple(lk), H, d, seed, k_offset)
+    return (w,) + W.make_kv_inputs(w)
+
+
+def run_kv(w, q, k, v, splits=0, scale=None, lse=True):
+    cq = torch.tensor(w.cu_q, device="cuda")
+    ck = torch.tensor(w.cu_k, device="cuda")
+    r = ts.ts_attn_fwd_kvcache(q.cuda(), k.cuda(), v.cuda(), cq, ck, w.max_q, w.max_k,
+                               scale=scale, return_lse=lse, num_splits=splits)
+    torch.cuda.synchronize()
+    if lse:
+        return r[0].cpu(), r[1].cpu()
+    return r.cpu(), None
+
+
+def oracle(w, q, k, v, scale):
+    return ts_ref.attn_kv_full(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), w.cu_q, w.cu_k, scale)
+
+
+def check_lse(got, ref, what):
+    got = got.double().numpy()
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(got), fin), what + ": -inf pattern differs"
+    assert np.all(got[~fin] == -np.inf), what
+    err = float(np.max(np.abs(got[fin] - ref[fin]))) if fin.any() else 0.0
+    assert err <= LSE_ABS, "%s: lse max-abs %.3g" % (what, err)
+    return err
+
+
+def as_f64(o):
+    return o.float().numpy().astype(np.float64)
+
+
+# segments: several query and key tiles, ragged tails, a segment without keys, one without queries,
+# a one-query segment and a one-key segment
+LQ = [100, 0, 300, 257, 1, 40]
+LK = [700, 50, 0, 1000, 64, 1]
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_kv_full(d):
+    w, q, k, v = draw(LQ, LK, 3, d, 31, k_offset=True)
+    say("kv full", d, LQ, LK)
+    o, lse = run_kv(w, q, k, v, splits=1)
+    ro, rlse = oracle(w, q, k, v, w.scale)
+    e = assert_parity(as_f64(o), ro, "kv full d=%d" % d)
+    le = check_lse(lse, rlse, "kv full d=%d" % d)
+    say("errors", e, "lse", le)
+    nokeys = slice(int(w.cu_q[2]), int(w.cu_q[3]))  # queries of the segment without keys
+    assert torch.all(o[nokeys].float() == 0.0)
+
+
+@pytest.mark.parametrize("splits", [2, 3, 7, 16])
+@pytest.mark.parametrize("d", [64, 128])
+def test_kv_forced_splits_full(splits, d):
+    w, q, k, v = draw(LQ, LK, 2, d, 41)
+    say("kv splits", splits, d)
+    o, lse = run_kv(w, q, k, v, splits=splits)
+    ro, rlse = oracle(w, q, k, v, w.scale)
+    assert_parity(as_f64(o), ro, "kv splits=%d d=%d" % (splits, d))
+    check_lse(lse, rlse, "kv splits=%d d=%d" % (splits, d))
+    # the split result differs from the unsplit one only by the rounding of the partials
+    o1, _ = run_kv(w, q, k, v, splits=1)
+    assert float((o.float() - o1.float()).abs().max()) <= 2e-2
+
+
+def test_kv_equal_offsets_is_varlen_bitwise():
+    lens = [300, 0, 1000, 65, 1]
+    w, q, k, v = draw(lens, lens, 2, 128, 51)
+    q = W.make_kv_inputs(w, seed=52)[0][: w.Tq]
+    say("kv == varlen", lens)
+    o_kv, lse = run_kv(w, q, k, v, splits=1)
+    cu = torch.tensor(w.cu_q, device="cuda")
+    o_var = ts.ts_attn_fwd_varlen(q.cuda(), k.cuda(), v.cuda(), cu, w.max_q)
+    torch.cuda.synchronize()
+    assert torch.equal(o_kv.view(torch.int16), o_var.cpu().view(torch.int16))
+    _, rlse = oracle(w, q, k, v, w.scale)
+    check_lse(lse, rlse, "kv == varlen")
+
+
+def test_kv_without_lse_matches_with_lse():
+    w, q, k, v = draw(LQ, LK, 2, 128, 61)
+    a, _ = run_kv(w, q, k, v, splits=1, lse=False)
+    b, _ = run_kv(w, q, k, v, splits=1, lse=True)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    c, _ = run_kv(w, q, k, v, splits=4, lse=False)
+    d, _ = run_kv(w, q, k, v, splits=4, lse=True)
+    assert torch.equal(c.view(torch.int16), d.view(torch.int16))
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.3, 0.9])
+def test_kv_other_scales(scale):
+    w, q, k, v = draw([70, 200], [500, 129], 2, 64, 71)
+    for splits in (1, 3):
+        o, lse = run_kv(w, q, k, v, splits=splits, scale=scale)
+        ro, rlse = oracle(w, q, k, v, scale)
+        assert_parity(as_f64(o), ro, "kv scale=%g splits=%d" % (scale, splits))
+        check_lse(lse, rlse, "kv scale=%g splits=%d" % (scale, splits))
+
+
+def test_kv_deterministic_bitwise():
+    w, q, k, v = draw(LQ, LK, 2, 128, 81)
+    for splits in (1, 5):
+        a, la = run_kv(w, q, k, v, splits=splits)
+        b, lb = run_kv(w, q, k, v, splits=splits)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        assert torch.equal(la.view(torch.int32), lb.view(torch.int32))
+
+
+@pytest.mark.parametrize("name,n_random", [("kv_chunk", 12), ("kv_chunk_1s", 48)])
+def test_kv_workload_sampled(name, n_random):
+    """The full chunk-vs-cache workloads in the configuration the benchmark times (automatic
+    splits), checked on sampled query rows of every head."""
+    w = W.KV_WORKLOADS[name]
+    q, k, v = W.make_kv_inputs(w)
+    say("kv workload", name, w.Tq, w.Tk, w.H)
+    o, lse = run_kv(w, q, k, v, splits=0)
+    row_t, row_h = W.sample_kv_rows(w, n_random=n_random)
+    ro, rlse = ts_ref.attn_kv_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), w.cu_q, w.cu_k,
+                                   w.scale, row_t, row_h)
+    got = as_f64(o[torch.from_numpy(row_t), torch.from_numpy(row_h.astype(np.int64))])
+    e = assert_parity(got, ro, name)
+    le = check_lse(lse[torch.from_numpy(row_t), torch.from_numpy(row_h.astype(np.int64))], rlse, name)
+    say(name, "errors", e, "lse", le)
+    assert float(np.abs(got).mean()) > 1e-3  # not an all-zero output
+
+
+def test_kv_bad_offsets_validate_mode():
+    w, q, k, v = draw([64, 64], [128, 128], 1, 64, 91)
+    cq = torch.tensor(w.cu_q, device="cuda")
+    bad_k = torch.tensor([0, 200, 256], dtype=torch.int32, device="cuda")  # segment longer than max_k
+    os.environ["TS_ATTN_VALIDATE"] = "1"
+    try:
+        with pytest.raises(ts.TsAttnError) as ei:
+            ts.ts_attn_fwd_kvcache(q.cuda(), k.cuda(), v.cuda(), cq, bad_k, w.max_q, 128)
+        assert ei.value.status == 10
+    finally:
+        del os.environ["TS_ATTN_VALIDATE"]
