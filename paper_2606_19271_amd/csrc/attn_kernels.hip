@@ -147,13 +147,20 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 // XCD-aware order: workgroup b runs on XCD b % 8; consecutive workgroups of one XCD take
 // `chunk` consecutive items, and every 8*chunk workgroups cover 8*chunk consecutive items,
-// so the global order is kept at that granularity.  Bijective on [0, total).
+// so the global order is kept at that granularity.  The r items after the last whole span are
+// dealt the same way: XCD x takes a contiguous block of its ceil((r - x) / 8) of them.
+// Bijective on [0, total).
 __device__ __forceinline__ int remap_block(int b, int total, int chunk) {
-  int span = 8 * chunk;
-  int full = (total / span) * span;
-  if (b >= full) return b;
-  int x = b & 7, j = b >> 3;
-  return (j / chunk) * span + x * chunk + (j % chunk);
+  const int span = 8 * chunk;
+  const int full = (total / span) * span;
+  const int x = b & 7;
+  if (b < full) {
+    const int j = b >> 3;
+    return (j / chunk) * span + x * chunk + (j % chunk);
+  }
+  const int r = total - full, j = (b - full) >> 3;  // j-th tail workgroup of XCD x
+  const int q = r >> 3, rem = r & 7;                // XCD x has q + (x < rem) of them
+  return full + x * q + min(x, rem) + j;
 }
 
 // S^T = K Q^T for one 64-key tile: two 32-key blocks, each an accumulation over d in steps of 16.

@@ -125,17 +125,23 @@ int check_kv(const void* q, const void* k, const void* v, const void* o, const f
   return TS_OK;
 }
 
-// Key ranges per query tile when the caller leaves the choice to the library: enough work
-// items for about two workgroups per CU, with at least 8 key tiles (512 keys) per range.
+// Key ranges per query tile when the caller leaves the choice to the library.  One 512-thread
+// workgroup runs per CU, so `items` work items take ceil(items / cus) rounds, each as long as
+// one item's key tiles.  Query tiles that already fill the GPU are not split (the partials would
+// only add traffic); otherwise n minimises rounds(items * n) * ceil(tiles / n), the smallest n
+// winning ties, with at least 4 key tiles per range.
 int32_t auto_splits(int cus, int32_t total_q, int32_t max_k, int32_t H) {
   const int64_t items = (int64_t)H * ((total_q + 255) / 256);
-  const int64_t target = 2 * (int64_t)cus;
-  if (items <= 0 || items >= target) return 1;
-  int64_t n = (target + items - 1) / items;
-  const int64_t cap = ((int64_t)max_k + 511) / 512;
-  if (n > cap) n = cap;
-  if (n > kMaxSplits) n = kMaxSplits;
-  return n < 1 ? 1 : (int32_t)n;
+  const int64_t tiles = ((int64_t)max_k + 63) / 64;
+  if (items <= 0 || items >= cus || tiles < 8) return 1;
+  int32_t best = 1;
+  int64_t best_cost = INT64_MAX;
+  for (int32_t n = 1; n <= kMaxSplits && tiles / n >= 4; ++n) {
+    const int64_t rounds = (items * n + cus - 1) / cus;
+    const int64_t cost = rounds * ((tiles + n - 1) / n);
+    if (cost < best_cost) { best_cost = cost; best = n; }
+  }
+  return best;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
