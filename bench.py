@@ -14,6 +14,10 @@ Other workloads (--workload): the dense and packed self-attention cases of workl
 and the chunk-vs-cache cases of workloads.KV_WORKLOADS (ts_attn_fwd_kvcache with the library's
 automatic key splits: flops = sum_s 4 Lq_s Lk_s d H; the events bracket the whole call, i.e. the
 planning, attention and, when split, merge kernels).
+--workload offload_kv times the session-state copy path instead: suspending the two largest
+sessions of the kv_chunk batch (their K and V rows, 1.25 GB) to pinned host memory with
+ts_state_copy (value = GB/s device -> host; the resume rate host -> device is reported beside it),
+against the host link's 64 GB/s per direction (PCIe 5.0 x16).
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--cpu-seconds S]
 """
 import argparse
@@ -96,6 +100,91 @@ def cpu_baseline(w, q, k, v, o_gpu, seconds):
     }, {"rows": int(done), "max_abs": float(err.max()), "mean_abs": float(err.mean())}
 
 
+PCIE5_X16_GBS = 64.0  # one direction, 32 GT/s x 16 lanes
+
+
+def bench_offload(args, torch, np, ts, W):
+    """Suspend / resume of session state: the K and V rows of two sessions of kv_chunk."""
+    w = W.KV_WORKLOADS["kv_chunk"]
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(w.seed)  # state bytes: any seeded pattern
+    row = w.H * w.d * 2
+    kd = torch.randint(-32768, 32767, (w.Tk * w.H * w.d,), generator=g, dtype=torch.int16, device=dev)
+    vd = torch.randint(-32768, 32767, (w.Tk * w.H * w.d,), generator=g, dtype=torch.int16, device=dev)
+    sessions = [4, 3]
+    rk, end_k = ts.pack_ranges(w.cu_k, sessions, row)
+    rv, end_v = ts.pack_ranges(w.cu_k, sessions, row, dst_start=end_k)
+    host = torch.empty(end_v, dtype=torch.uint8, pin_memory=True)
+    kb, vb = kd.view(torch.uint8), vd.view(torch.uint8)
+    k_back, v_back = torch.empty_like(kb), torch.empty_like(vb)
+    back_k = [(d, s, n) for s, d, n in rk]
+    back_v = [(d, s, n) for s, d, n in rv]
+
+    def offload():
+        ts.ts_state_copy(kb, host, rk)
+        ts.ts_state_copy(vb, host, rv)
+
+    def resume():
+        ts.ts_state_copy(host, k_back, back_k)
+        ts.ts_state_copy(host, v_back, back_v)
+
+    def timed(fn, steps):
+        stream = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps, e0.elapsed_time(e1) * 1e-3 / steps
+
+    for _ in range(args.warmup):
+        offload()
+        resume()
+    wall_off, ev_off = timed(offload, args.steps)
+    wall_res, ev_res = timed(resume, args.steps)
+    nbytes = end_v
+    ok = bool(torch.equal(k_back[rk[0][0]:rk[0][0] + rk[0][2]], kb[rk[0][0]:rk[0][0] + rk[0][2]]))
+
+    # context: the driver's copy engine on the same contiguous bytes (hipMemcpyAsync)
+    def sdma():
+        for (s0, d0, n), src in [(r, kb) for r in rk] + [(r, vb) for r in rv]:
+            host[d0:d0 + n].copy_(src[s0:s0 + n], non_blocking=True)
+    sdma()
+    wall_sdma, _ = timed(sdma, max(1, args.steps // 2))
+
+    result = {
+        "metric": "session-state offload GB/s (K and V rows of 2 sessions, device -> pinned host)",
+        "value": nbytes / wall_off / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall_off * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "config": {"workload": "offload_kv", "sessions": sessions,
+                   "keys": [w.k_seqlens[s] for s in sessions], "H": w.H, "d": w.d,
+                   "bytes_per_step": nbytes, "resume_GBps": nbytes / wall_res / 1e9,
+                   "hipMemcpyAsync_offload_GBps": nbytes / wall_sdma / 1e9,
+                   "round_trip_exact": ok},
+        "roofline": {"bound": "host-link", "achieved": nbytes / ev_off / 1e9,
+                     "peak": PCIE5_X16_GBS, "unit": "GB/s",
+                     "frac": nbytes / ev_off / 1e9 / PCIE5_X16_GBS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import state_copy as SC
+        n_sample = 256 << 20
+        src = np.random.default_rng(1).integers(0, 256, n_sample, dtype=np.uint8)
+        dst = np.zeros(n_sample, np.uint8)
+        t0, done = time.perf_counter(), 0
+        while time.perf_counter() - t0 < min(args.cpu_seconds, 5.0):
+            SC.copy_ranges(src, dst, [(0, 0, n_sample)])
+            done += n_sample
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": done / dt / 1e9, "unit": "GB/s", "cores": 1,
+                                  "kind": "oracle",
+                                  "sample": "numpy range copy of 256 MiB host -> host, %.1f s" % dt}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,6 +227,9 @@ def main():
         return
 
     kv = args.workload in W.KV_WORKLOADS
+    if args.workload == "offload_kv":
+        bench_offload(args, torch, np, ts, W)
+        return
     w = W.KV_WORKLOADS[args.workload] if kv else W.WORKLOADS[args.workload]
     q, k, v = W.make_kv_inputs(w) if kv else W.make_inputs(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)

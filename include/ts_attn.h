@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 2
+#define TS_ATTN_ABI_VERSION 3
 
 typedef enum ts_status {
   TS_OK = 0,
@@ -63,7 +63,8 @@ typedef enum ts_status {
   TS_ERR_UNSUPPORTED = 7, /* no usable gfx950 device */
   TS_ERR_HIP = 8,         /* a HIP runtime call or kernel launch failed */
   TS_ERR_NOMEM = 9,       /* device scratch allocation failed */
-  TS_ERR_SEGMENTS = 10    /* cu_seqlens contents invalid (reported only in validation mode) */
+  TS_ERR_SEGMENTS = 10,   /* cu_seqlens contents invalid (reported only in validation mode) */
+  TS_ERR_MEMORY = 11      /* a copy operand is neither current-device memory nor pinned host memory */
 } ts_status;
 
 /*
@@ -135,6 +136,31 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                         int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
                         int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits,
                         void* stream);
+
+/*
+ * Session-state copy: suspend (device -> host), resume (host -> device) and compaction (device
+ * -> device) of session state regions.  The paper's runtime suspends an idle session by copying
+ * its persistent state from GPU memory to host memory and resumes it by restoring that state to
+ * the GPU chosen for it (Sec. 3.1, "GPU-CPU state offloading"); only the session's isolated
+ * state region moves (Sec. 6.1, "Session memory layout").  In a packed token-major batch a
+ * session's cached keys (or values) are one contiguous byte range, rows
+ * [cu_seqlens_k[s], cu_seqlens_k[s+1]) times H * d * 2 bytes.
+ *   for every r < nranges:  dst[ranges[3r+1] .. + ranges[3r+2]) = src[ranges[3r] .. + ranges[3r+2])
+ *  src, dst     base pointers: device memory of the current device, or pinned host memory
+ *               (page-locked and mapped, e.g. hipHostMalloc or torch pin_memory); 16-byte
+ *               aligned.  Pageable, managed or another device's memory gives TS_ERR_MEMORY.
+ *  src_bytes,   sizes of the src and dst buffers; every range must lie inside them
+ *  dst_bytes    (TS_ERR_SHAPE otherwise).  The two buffers must not overlap (TS_ERR_ALIAS);
+ *               ranges whose destinations overlap each other leave those bytes unspecified.
+ *  ranges       HOST array of 3 * nranges int64: source offset, destination offset, byte count
+ *               of each range, all multiples of 16 (TS_ERR_ALIGN) and non-negative.  Read during
+ *               the call only.
+ * One kernel launch per 64 ranges on stream, asynchronous like every entry point: host memory
+ * written by a suspend is complete once the stream reaches that point (synchronize before
+ * reading it).  No device memory is allocated.  nranges = 0 is a no-op.
+ */
+int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_bytes,
+                  const int64_t* ranges, int32_t nranges, void* stream);
 
 /* Human-readable name of a ts_status value (a static string; never NULL). */
 const char* ts_attn_status_str(int status);

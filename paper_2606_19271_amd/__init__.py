@@ -6,6 +6,7 @@ include/ts_attn.h); this package only marshals torch tensors into that ABI.
 from .attention import (ts_attn_fwd, ts_attn_fwd_kvcache, ts_attn_fwd_varlen,  # noqa: F401
                         default_scale)
 from ._lib import TsAttnError, load, status_str  # noqa: F401
+from .state import pack_ranges, ts_state_copy  # noqa: F401
 
 
 def abi_version():

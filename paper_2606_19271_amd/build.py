@@ -7,7 +7,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libts_attn.so")
-SOURCES = [os.path.join(CSRC, "attn_kernels.hip"), os.path.join(CSRC, "ts_attn.cpp")]
+SOURCES = [os.path.join(CSRC, "attn_kernels.hip"), os.path.join(CSRC, "state_copy.hip"),
+           os.path.join(CSRC, "ts_attn.cpp")]
 
 # Packed fp32 VALU instructions are kept out of the generated code on purpose.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

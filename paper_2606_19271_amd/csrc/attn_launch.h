@@ -45,6 +45,22 @@ int64_t plan_ints(int32_t nseq);
 // Queries per work item.
 int query_tile();
 
+// Up to kMaxCopyRanges byte-range copies of one state-copy launch (passed by value as a kernel
+// argument): range r copies bytes[r] bytes from src + src[r] to dst + dst[r]; first_chunk is the
+// prefix over the ranges of ceil(bytes / copy_chunk_bytes()), first_chunk[n] = chunks in all.
+constexpr int kMaxCopyRanges = 64;
+struct CopyList {
+  int64_t src[kMaxCopyRanges];
+  int64_t dst[kMaxCopyRanges];
+  int64_t bytes[kMaxCopyRanges];
+  int64_t first_chunk[kMaxCopyRanges + 1];
+  int32_t n;
+};
+int64_t copy_chunk_bytes();
+// src_host / dst_host: that side is pinned host memory (accessed non-temporally).
+hipError_t launch_state_copy(const void* src, void* dst, const CopyList& list, bool src_host,
+                             bool dst_host, hipStream_t st);
+
 hipError_t configure_kernels();
 hipError_t launch_dense(const DenseArgs& a, hipStream_t st);
 hipError_t launch_packed(const PackedArgs& a, hipStream_t st);

@@ -176,6 +176,30 @@ int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
   return rc;
 }
 
+// Device-visible address of a copy operand: device memory of the current device, or pinned
+// (page-locked, mapped) host memory.  Anything else -- pageable host memory, managed memory,
+// another device's memory -- is refused, since the copy kernel would fault on it.
+int copy_operand(const void* p, int dev, const void** devp, bool* host) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();  // clear the error this lookup leaves behind
+    return TS_ERR_MEMORY;
+  }
+  if (a.type == hipMemoryTypeDevice && a.device == dev) {
+    *devp = p;
+    *host = false;
+    return TS_OK;
+  }
+  if (a.type == hipMemoryTypeHost && a.devicePointer != nullptr) {
+    const char* base_h = (const char*)a.hostPointer;
+    const char* base_d = (const char*)a.devicePointer;
+    *devp = base_h ? base_d + ((const char*)p - base_h) : base_d;
+    *host = true;
+    return TS_OK;
+  }
+  return TS_ERR_MEMORY;
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +219,7 @@ const char* ts_attn_status_str(int status) {
     case TS_ERR_HIP: return "TS_ERR_HIP: HIP runtime or launch failure";
     case TS_ERR_NOMEM: return "TS_ERR_NOMEM: device scratch allocation failed";
     case TS_ERR_SEGMENTS: return "TS_ERR_SEGMENTS: invalid cu_seqlens contents";
+    case TS_ERR_MEMORY: return "TS_ERR_MEMORY: pointer is neither device memory of the current device nor pinned host memory";
     default: return "unknown ts_status";
   }
 }
@@ -248,6 +273,50 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                        max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
   return run_packed(st, a, (hipStream_t)stream);
+}
+
+int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_bytes,
+                  const int64_t* ranges, int32_t nranges, void* stream) {
+  if (nranges < 0 || src_bytes < 0 || dst_bytes < 0) return TS_ERR_SHAPE;
+  if (nranges == 0) return TS_OK;
+  if (!src || !dst || !ranges) return TS_ERR_NULL;
+  if (misaligned(src) || misaligned(dst)) return TS_ERR_ALIGN;
+  if (ranges_overlap(src, src_bytes, dst, dst_bytes)) return TS_ERR_ALIAS;
+  for (int32_t r = 0; r < nranges; ++r) {
+    const int64_t so = ranges[3 * r], d_o = ranges[3 * r + 1], n = ranges[3 * r + 2];
+    if (so < 0 || d_o < 0 || n < 0) return TS_ERR_SHAPE;
+    if (((so | d_o | n) & 15) != 0) return TS_ERR_ALIGN;
+    if (so > src_bytes || n > src_bytes - so || d_o > dst_bytes || n > dst_bytes - d_o)
+      return TS_ERR_SHAPE;
+  }
+  int rc = TS_OK;
+  DeviceState* st = current_device(&rc);
+  if (!st) return rc;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return TS_ERR_HIP;
+  const void* s_dev = nullptr;
+  const void* d_dev = nullptr;
+  bool s_host = false, d_host = false;
+  if ((rc = copy_operand(src, dev, &s_dev, &s_host)) != TS_OK) return rc;
+  if ((rc = copy_operand(dst, dev, &d_dev, &d_host)) != TS_OK) return rc;
+  const int64_t chunk = tsattn::copy_chunk_bytes();
+  tsattn::CopyList list;
+  for (int32_t r0 = 0; r0 < nranges; r0 += tsattn::kMaxCopyRanges) {
+    list.n = nranges - r0 < tsattn::kMaxCopyRanges ? nranges - r0 : tsattn::kMaxCopyRanges;
+    list.first_chunk[0] = 0;
+    for (int32_t i = 0; i < list.n; ++i) {
+      const int64_t* e = ranges + 3 * (int64_t)(r0 + i);
+      list.src[i] = e[0];
+      list.dst[i] = e[1];
+      list.bytes[i] = e[2];
+      list.first_chunk[i + 1] = list.first_chunk[i] + (e[2] + chunk - 1) / chunk;
+    }
+    if (list.first_chunk[list.n] >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
+    if (tsattn::launch_state_copy(s_dev, (void*)d_dev, list, s_host, d_host, (hipStream_t)stream) !=
+        hipSuccess)
+      return TS_ERR_HIP;
+  }
+  return TS_OK;
 }
 
 }  // extern "C"

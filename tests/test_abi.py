@@ -6,6 +6,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -35,11 +36,15 @@ def test_exports_every_declared_symbol(lib):
     names = declared_functions()
     assert names == ["ts_attn_abi_version", "ts_attn_fwd", "ts_attn_fwd_kvcache",
                      "ts_attn_fwd_varlen", "ts_attn_status_str"]
+    copy_names = sorted(set(re.findall(r"\b(ts_state_\w+)\s*\(",
+                                       re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S))))
+    assert copy_names == ["ts_state_copy"]
+    names = names + copy_names
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB], capture_output=True, text=True,
                          check=True).stdout
-    exported = set(re.findall(r"\bT (ts_attn_\w+)", out))
+    exported = set(re.findall(r"\bT (ts_\w+)", out))
     assert set(names) <= exported
 
 
@@ -140,6 +145,32 @@ def test_kvcache_argument_checks(lib):
     # empty problems are no-ops that never touch the device
     assert kvcache(lib, nseq=0) == _lib.TS_OK
     assert kvcache(lib, tq=0) == _lib.TS_OK
+
+
+def state_copy(lib, src=A, sb=1 << 20, dst=BIG, db=1 << 20, ranges=((0, 0, 256),), n=None):
+    r = np.ascontiguousarray(np.asarray(ranges, dtype=np.int64).reshape(-1, 3))
+    P = ctypes.c_void_p
+    return lib.ts_state_copy(P(src), sb, P(dst), db, P(r.ctypes.data), r.shape[0] if n is None else n,
+                             P(None))
+
+
+def test_state_copy_argument_checks(lib):
+    assert state_copy(lib, n=-1) == _lib.TS_ERR_SHAPE
+    assert state_copy(lib, n=0) == _lib.TS_OK
+    assert state_copy(lib, src=0) == _lib.TS_ERR_NULL
+    assert state_copy(lib, dst=A + 8) == _lib.TS_ERR_ALIGN
+    assert state_copy(lib, ranges=((16, 0, 24),)) == _lib.TS_ERR_ALIGN
+    assert state_copy(lib, ranges=((0, 8, 16),)) == _lib.TS_ERR_ALIGN
+    assert state_copy(lib, ranges=((-16, 0, 16),)) == _lib.TS_ERR_SHAPE
+    assert state_copy(lib, ranges=((0, 0, (1 << 20) + 16),)) == _lib.TS_ERR_SHAPE   # past src
+    assert state_copy(lib, ranges=((0, (1 << 20) - 16, 32),)) == _lib.TS_ERR_SHAPE  # past dst
+    assert state_copy(lib, dst=A + 4096) == _lib.TS_ERR_ALIAS                     # buffers overlap
+
+
+def test_pack_ranges():
+    r, end = ts.pack_ranges([0, 7, 7, 19, 30], [3, 1, 0], 80, dst_start=160)
+    assert r == [(19 * 80, 160, 11 * 80), (7 * 80, 160 + 880, 0), (0, 1040, 7 * 80)]
+    assert end == 1040 + 560
 
 
 def test_python_binding_rejects_cpu_tensors():
