@@ -208,3 +208,100 @@ def sample_rows(w, n_random=64, seed=None):
     row_t = np.tile(ts, w.H)
     row_h = np.repeat(np.arange(w.H, dtype=np.int32), ts.size)
     return row_t, row_h
+
+
+# ---- session event traces for the closed-loop scheduler ------------------------------------
+# Event codes of one session change; the values are the ones of the scheduler's C ABI.
+EV_ARRIVE, EV_DEPART, EV_ACTIVATE, EV_IDLE = 0, 1, 2, 3
+
+# Per-minute arrivals and departures of the six evaluation traces of the paper (appendix of
+# workload statistics, table of evaluated trace characteristics): T1-T3 ran on the H20 cluster,
+# T4-T6 on the B300 cluster.  The traces themselves are not public; only these aggregates are.
+TRACE_TABLE = {
+    "T1": ((122, 130, 66, 22, 18), (44, 86, 88, 64, 38)),
+    "T2": ((218, 214, 248, 192, 204), (60, 124, 204, 196, 204)),
+    "T3": ((74, 148, 156, 264, 156), (10, 64, 126, 148, 214)),
+    "T4": ((500, 428, 308, 88, 80), (158, 266, 388, 236, 152)),
+    "T5": ((874, 862, 998, 762, 814), (238, 504, 810, 784, 814)),
+    "T6": ((296, 590, 626, 1062, 618), (36, 260, 502, 608, 846)),
+}
+
+
+def session_trace(n_epochs, seed, mean_arrivals=1.0, burst_every=0, burst=0, p_idle=0.1,
+                  p_resume=0.3, p_depart=0.05, state_bytes=(0, 1)):
+    """A seeded stream of decision epochs; each epoch is a list of (kind, session id, state bytes).
+
+    Per epoch, in this order: every live session may depart (p_depart); an active one that stays
+    may go idle (p_idle); an idle one may become active again (p_resume); then Poisson
+    (mean_arrivals) new sessions arrive, plus `burst` more on every `burst_every`-th epoch.  Ids
+    increase with arrival; state sizes are uniform integers in [state_bytes[0], state_bytes[1])."""
+    rng = np.random.default_rng(seed)
+    active, idle, out, nid = [], [], [], 0
+    for t in range(n_epochs):
+        ch, nxt_active, nxt_idle = [], [], []
+        for i in active:
+            if rng.random() < p_depart:
+                ch.append((EV_DEPART, i, 0))
+            elif rng.random() < p_idle:
+                ch.append((EV_IDLE, i, 0)); nxt_idle.append(i)
+            else:
+                nxt_active.append(i)
+        for i in idle:
+            if rng.random() < p_depart:
+                ch.append((EV_DEPART, i, 0))
+            elif rng.random() < p_resume:
+                ch.append((EV_ACTIVATE, i, 0)); nxt_active.append(i)
+            else:
+                nxt_idle.append(i)
+        n_new = int(rng.poisson(mean_arrivals))
+        if burst_every and t % burst_every == burst_every - 1:
+            n_new += burst
+        for _ in range(n_new):
+            ch.append((EV_ARRIVE, nid, int(rng.integers(state_bytes[0], state_bytes[1]))))
+            nxt_active.append(nid)
+            nid += 1
+        active, idle = sorted(nxt_active), sorted(nxt_idle)
+        out.append(ch)
+    return out
+
+
+def table_trace(name, seed, bins_per_minute=12, scale=1.0, p_idle=0.05, p_resume=0.5,
+                concentration=0.5, state_bytes=(0, 1)):
+    """Decision epochs of 60/bins_per_minute seconds shaped like one trace of TRACE_TABLE: each
+    minute's arrivals and departures (times `scale`, rounded) are spread over its bins with
+    Dirichlet(concentration) weights (smaller = burstier); a departure takes a random live session
+    that arrived in an earlier epoch (deferred while none is live); live sessions flip between
+    active and idle with p_idle / p_resume per epoch."""
+    rng = np.random.default_rng(seed)
+    arr_min, dep_min = TRACE_TABLE[name]
+    active, idle, out, nid, owed = [], [], [], 0, 0
+    for a_m, d_m in zip(arr_min, dep_min):
+        a_bins = rng.multinomial(int(round(a_m * scale)), rng.dirichlet([concentration] * bins_per_minute))
+        d_bins = rng.multinomial(int(round(d_m * scale)), rng.dirichlet([concentration] * bins_per_minute))
+        for b in range(bins_per_minute):
+            ch = []
+            owed += int(d_bins[b])
+            while owed and (active or idle):
+                live = active + idle
+                i = live[int(rng.integers(len(live)))]
+                (active if i in active else idle).remove(i)
+                ch.append((EV_DEPART, i, 0))
+                owed -= 1
+            nxt_active, nxt_idle = [], []
+            for i in active:
+                if rng.random() < p_idle:
+                    ch.append((EV_IDLE, i, 0)); nxt_idle.append(i)
+                else:
+                    nxt_active.append(i)
+            for i in idle:
+                if rng.random() < p_resume:
+                    ch.append((EV_ACTIVATE, i, 0)); nxt_active.append(i)
+                else:
+                    nxt_idle.append(i)
+            for _ in range(int(a_bins[b])):
+                ch.append((EV_ARRIVE, nid, int(rng.integers(state_bytes[0], state_bytes[1]))))
+                nxt_active.append(nid)
+                nid += 1
+            active, idle = sorted(nxt_active), sorted(nxt_idle)
+            out.append(ch)
+    return out
