@@ -169,12 +169,14 @@ class SchedRef:
     def apply_changes(self, changes):
         """Validates all changes against a copy first, so an invalid epoch changes nothing."""
         active, byts = dict(self.active), dict(self.bytes)
+        fresh = set()          # sessions that arrived in this epoch: they hold no GPU yet
         a_t = 0
         for kind, i, nbytes in changes:
             if kind == ARRIVE:
                 if i in active or nbytes < 0:
                     raise SchedError(f"bad arrival of session {i}")
                 active[i], byts[i] = True, nbytes
+                fresh.add(i)
                 a_t += 1
             elif kind == DEPART:
                 if i not in active:
@@ -191,8 +193,9 @@ class SchedRef:
                 active[i] = False
             else:
                 raise SchedError(f"unknown event kind {kind}")
-        # initialise from phi(t-): departed sessions vanish, idle ones are suspended (R1)
-        self.phi = {i: (self.phi.get(i) if active[i] else None) for i in active}
+        # initialise from phi(t-): departed sessions vanish, idle ones are suspended (R1); a
+        # session that went idle and came back within the epoch keeps its GPU
+        self.phi = {i: (self.phi.get(i) if active[i] and i not in fresh else None) for i in active}
         self.active, self.bytes = active, byts
         return a_t
 

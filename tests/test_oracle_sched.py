@@ -296,6 +296,20 @@ def pin_parameter_delay(mod):
     assert d["m"] == 3 and sorted(len(v) for v in groups(s).values()) == [1, 1, 1]
 
 
+def pin_changes_within_one_epoch(mod):
+    """Changes of one epoch take effect together: idle-and-back keeps the GPU, a session that
+    departs and re-arrives under the same id is a new session, arrive-then-idle never holds a GPU."""
+    s = make(mod, m_min=2, m_max=2, m_init=2, alpha=1000.0)
+    s.step(arrive(1, 2, 3))                               # g0 = {1,3}, g1 = {2}
+    d = s.step(ev(SR.IDLE, 1) + ev(SR.ACTIVATE, 1))
+    assert groups(s) == {0: [1, 3], 1: [2]} and (d["placed"], s.history[-1]) == (0, 1)
+    # the new session 3 is placed afresh: g0 and g1 both give 200 with equal loads -> g0
+    d = s.step(ev(SR.DEPART, 3) + arrive(3))
+    assert groups(s) == {0: [1, 3], 1: [2]} and d["placed"] == 1
+    d = s.step(arrive(4) + ev(SR.IDLE, 4))
+    assert dict(s.placement())[4] == -1 and d["placed"] == 0 and d["n_req"] == 3
+
+
 def pin_invalid_changes(mod):
     s = make(mod)
     s.step(arrive(1, 2) + ev(SR.IDLE, 2))
@@ -333,7 +347,8 @@ def pin_invariants(mod):
 PINS = [pin_app_a_table, pin_volatility_numpy, pin_activations_count, pin_target_budget,
         pin_placement_optimal, pin_assignment_and_gain, pin_assignment_prefers_less_loaded,
         pin_hysteresis_band, pin_migration_cost_blocks,
-        pin_closed_loop_trace, pin_pending_when_full, pin_parameter_delay, pin_invalid_changes,
+        pin_closed_loop_trace, pin_pending_when_full, pin_parameter_delay,
+        pin_changes_within_one_epoch, pin_invalid_changes,
         pin_invariants]
 
 
@@ -372,7 +387,8 @@ MUTANTS = {
     "sample_std": ("statistics.pstdev(window)", "statistics.stdev(window)"),
     "rho_level_index": ("self.rho_tab[self.level - 1]", "self.rho_tab[min(self.level, len(self.rho_tab) - 1)]"),
     "activate_not_counted": ("active[i] = True\n                a_t += 1", "active[i] = True"),
-    "idle_not_suspended": ("(self.phi.get(i) if active[i] else None)", "self.phi.get(i)"),
+    "idle_not_suspended": ("(self.phi.get(i) if active[i] and i not in fresh else None)",
+                           "(self.phi.get(i) if i not in fresh else None)"),
     "update_before_scale": [("        a_t = self.apply_changes(changes)\n",
                              "        a_t = self.apply_changes(changes)\n        self.update_parameters(a_t)\n"),
                             ("        self.update_parameters(a_t)\n        return {", "        return {")],
