@@ -1,0 +1,274 @@
+"""The scheduler library (libts_sched.so, include/ts_sched.h) against the oracle
+(oracle/sched_ref.py): every decision of every epoch, every placement and every GPU list must be
+identical -- integers and doubles bit for bit -- on seeded synthetic traces, plus the hand-derived
+traces of the oracle's pins, argument validation, and the ABI surface.  Host code only."""
+import ctypes
+import itertools
+import json
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import sched_ref as SR
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ts_sched.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "app_a_volatility_levels.json")
+TABLE = json.load(open(GOLDEN))["levels"]
+
+sched = pytest.importorskip("paper_2606_19271_amd.sched")
+
+LAT4 = [0.0, 150.0, 200.0, 260.0, 330.0]
+
+
+def latency(K, base=100.0, slope=40.0, curve=6.0):
+    """A convex per-chunk latency table l(0..K) in ms (co-location slows every session)."""
+    return [0.0] + [base + slope * n + curve * n * n for n in range(1, K + 1)]
+
+
+def app_a_levels():
+    vols = [r["volatility"] for r in TABLE]
+    return dict(level_bound=SR.level_bounds_from_table(vols),
+                level_lambda=[r["lambda"] for r in TABLE], level_rho=[r["rho"] for r in TABLE])
+
+
+def pair(K, m_min, m_max, m_init, lat, eta, alpha=0.0, beta=0.0, delta=0.1, window=8,
+         level_bound=(), level_lambda=(0.2,), level_rho=(0.5,)):
+    lib = sched.Scheduler(K, m_min, m_max, m_init, lat, eta, alpha, beta, delta, window,
+                          list(level_bound), list(level_lambda), list(level_rho))
+    ref = SR.SchedRef(K, m_min, m_max, m_init, lat, eta, alpha, beta, delta, window,
+                      list(level_bound), list(level_lambda), list(level_rho))
+    return lib, ref
+
+
+def same_decision(a, b):
+    for k in sched.DECISION_KEYS:
+        x, y = a[k], b[k]
+        if isinstance(y, float) and isinstance(x, float):
+            if not (x == y or (math.isnan(x) and math.isnan(y))) or math.copysign(1, x) != math.copysign(1, y):
+                return False
+        elif x != y:
+            return False
+    return True
+
+
+def run_both(lib, ref, trace):
+    for t, ch in enumerate(trace):
+        a, b = lib.step(ch), ref.step(ch)
+        assert same_decision(a, b), (t, a, b)
+        assert lib.placement() == ref.placement(), t
+        assert lib.gpu_loads() == ref.gpu_loads(), t
+    return t + 1
+
+
+CONFIGS = [
+    # (name, parameters, trace)
+    ("app_a_K4", dict(K=4, m_min=1, m_max=12, m_init=2, lat=LAT4, eta=0.05, alpha=5.0, beta=2e-9,
+                      delta=0.1, window=12, **app_a_levels()),
+     lambda: W.session_trace(160, seed=1, mean_arrivals=1.2, burst_every=15, burst=9, p_idle=0.1,
+                             p_resume=0.3, p_depart=0.04, state_bytes=(10 ** 9, 3 * 10 ** 9))),
+    ("free_moves_K8", dict(K=8, m_min=0, m_max=10, m_init=0, lat=latency(8), eta=1.0,
+                           delta=0.05, window=6, level_rho=(0.7,)),
+     lambda: W.session_trace(150, seed=2, mean_arrivals=2.0, burst_every=20, burst=12,
+                             p_idle=0.15, p_resume=0.25, p_depart=0.05)),
+    ("tied_costs_K6", dict(K=6, m_min=2, m_max=8, m_init=3, lat=latency(6, curve=0.0), eta=1.0,
+                           alpha=10.0, beta=1e-3, delta=0.15, window=5,
+                           level_bound=(0.6, 1.4), level_lambda=(0.1, 0.2, 0.4),
+                           level_rho=(0.9, 0.65, 0.4)),
+     lambda: W.session_trace(150, seed=3, mean_arrivals=1.5, burst_every=9, burst=6, p_idle=0.2,
+                             p_resume=0.3, p_depart=0.06, state_bytes=(0, 40000))),
+    ("flat_latency_K3", dict(K=3, m_min=1, m_max=6, m_init=1, lat=[0.0, 200.0, 200.0, 260.0],
+                             eta=0.5, beta=1e-6, delta=0.0, window=4, level_rho=(0.95,)),
+     lambda: W.session_trace(150, seed=4, mean_arrivals=0.9, burst_every=11, burst=5,
+                             p_idle=0.25, p_resume=0.4, p_depart=0.05, state_bytes=(0, 10 ** 7))),
+    ("capped_K2", dict(K=2, m_min=1, m_max=3, m_init=1, lat=[0.0, 100.0, 180.0], eta=1.0,
+                       delta=0.1, window=3, level_rho=(0.5,)),
+     lambda: W.session_trace(120, seed=5, mean_arrivals=1.0, burst_every=7, burst=4, p_idle=0.2,
+                             p_resume=0.3, p_depart=0.1)),
+    ("K1", dict(K=1, m_min=0, m_max=7, m_init=0, lat=[0.0, 100.0], eta=1.0, delta=0.2,
+                window=4, level_rho=(1.0,)),
+     lambda: W.session_trace(100, seed=6, mean_arrivals=0.7, p_idle=0.2, p_resume=0.3,
+                             p_depart=0.1)),
+    ("table_T1_small", dict(K=4, m_min=1, m_max=16, m_init=4, lat=LAT4, eta=0.05, alpha=20.0,
+                            beta=1e-9, delta=0.1, window=12, **app_a_levels()),
+     lambda: W.table_trace("T1", seed=7, scale=0.35, state_bytes=(10 ** 9, 3 * 10 ** 9))),
+]
+
+
+@pytest.mark.parametrize("name,prm,trace", CONFIGS, ids=[c[0] for c in CONFIGS])
+def test_library_matches_oracle_on_traces(name, prm, trace):
+    lib, ref = pair(**prm)
+    tr = trace()
+    n = run_both(lib, ref, tr)
+    assert n == len(tr)
+    assert sum(len(ch) for ch in tr) > 50
+
+
+def test_library_matches_oracle_with_within_epoch_changes():
+    """Idle-and-back, depart-and-re-arrive and arrive-then-idle within one epoch."""
+    lib, ref = pair(K=3, m_min=1, m_max=5, m_init=2, lat=[0.0, 100.0, 150.0, 230.0], eta=1.0,
+                    beta=1e-4)
+    rng = np.random.default_rng(8)
+    live, trace, nid = {}, [], 0
+    for t in range(120):
+        ch = []
+        for i in sorted(live):
+            r = rng.random()
+            if r < 0.08:
+                ch.append((SR.DEPART, i, 0))
+                if rng.random() < 0.5:   # the same id comes back as a new session
+                    ch.append((SR.ARRIVE, i, int(rng.integers(0, 5000))))
+                    live[i] = True
+                else:
+                    del live[i]
+            elif r < 0.2 and live[i]:
+                ch.append((SR.IDLE, i, 0))
+                if rng.random() < 0.5:
+                    ch.append((SR.ACTIVATE, i, 0))
+                else:
+                    live[i] = False
+            elif r < 0.35 and not live[i]:
+                ch.append((SR.ACTIVATE, i, 0)); live[i] = True
+        for _ in range(int(rng.poisson(0.8))):
+            ch.append((SR.ARRIVE, nid, int(rng.integers(0, 5000))))
+            if rng.random() < 0.2:
+                ch.append((SR.IDLE, nid, 0)); live[nid] = False
+            else:
+                live[nid] = True
+            nid += 1
+        trace.append(ch)
+    run_both(lib, ref, trace)
+
+
+def test_hand_derived_closed_loop_trace():
+    """The oracle's hand-derived Alg. 1 trace (K = 4, rho* 0.5, delta 0.1), on the library."""
+    lib = sched.Scheduler(4, 1, 8, 1, LAT4, 1.0, 0.0, 0.0, 0.1, 8, [], [0.2], [0.5])
+    A = lambda *ids: [(SR.ARRIVE, i, 0) for i in ids]  # noqa: E731
+    E = lambda k, *ids: [(k, i, 0) for i in ids]       # noqa: E731
+
+    def groups():
+        out = {g: [] for g, _ in lib.gpu_loads()}
+        for i, g in lib.placement():
+            if g >= 0:
+                out[g].append(i)
+        return out
+    assert lib.step(A(1))["m"] == 1
+    d = lib.step(A(2, 3))
+    assert (d["m"], d["migrations"], groups()) == (2, 1, {0: [2, 3], 1: [1]})
+    lib.step(A(4))
+    d = lib.step(A(5))
+    assert (d["m"], groups()) == (3, {0: [3, 5], 1: [1, 4], 2: [2]})
+    d = lib.step(E(SR.IDLE, 1, 3, 5))
+    assert (d["m"], d["placed"], d["migrations"], groups()) == (1, 0, 1, {1: [2, 4]})
+    d = lib.step(E(SR.ACTIVATE, 1, 3, 5))
+    assert (d["m"], d["placed"], d["migrations"], d["pending"]) == (3, 3, 2, 0)
+    assert groups() == {1: [3, 4], 3: [1, 5], 4: [2]}
+
+
+def test_pending_and_infinite_load_signal():
+    lib = sched.Scheduler(2, 1, 1, 1, [0.0, 100.0, 150.0], 1.0)
+    d = lib.step([(SR.ARRIVE, i, 0) for i in (1, 2, 3)])
+    assert d["pending"] == 1 and d["rho_max"] == math.inf and d["m"] == 1
+    d = lib.step([(SR.DEPART, 1, 0)])
+    assert d["pending"] == 0 and d["rho_max"] == 1.0 and dict(lib.placement()) == {2: 0, 3: 0}
+
+
+def test_invalid_changes_leave_the_state_unchanged():
+    lib = sched.Scheduler(4, 1, 8, 1, LAT4, 1.0, level_rho=(0.5,))
+    lib.step([(SR.ARRIVE, 1, 0), (SR.ARRIVE, 2, 0), (SR.IDLE, 2, 0)])
+    before = (lib.placement(), lib.gpu_loads())
+    cases = [([(SR.ARRIVE, 3, 0), (SR.ARRIVE, 1, 0)], 2), ([(SR.ARRIVE, 3, 0), (SR.IDLE, 2, 0)], 2),
+             ([(SR.ACTIVATE, 1, 0)], 2), ([(SR.DEPART, 9, 0)], 2), ([(7, 1, 0)], 1),
+             ([(SR.ARRIVE, 4, -1)], 2)]
+    for changes, status in cases:
+        with pytest.raises(sched.SchedError) as e:
+            lib.step(changes)
+        assert e.value.status == status
+        assert (lib.placement(), lib.gpu_loads()) == before
+    # the volatility window did not see the refused epochs either
+    ref = SR.SchedRef(4, 1, 8, 1, LAT4, 1.0, 0.0, 0.0, 0.1, 8, [], [0.2], [0.5])
+    ref.step([(SR.ARRIVE, 1, 0), (SR.ARRIVE, 2, 0), (SR.IDLE, 2, 0)])
+    assert same_decision(lib.step([]), ref.step([]))
+
+
+@pytest.mark.parametrize("bad", [
+    dict(K=0), dict(K=65), dict(m_min=-1), dict(m_max=0, m_init=1), dict(m_init=9),
+    dict(lat=[0.0, 150.0, 140.0, 260.0, 330.0]), dict(lat=[0.0, 150.0, math.inf, 260.0, 330.0]),
+    dict(eta=0.0), dict(eta=math.nan), dict(alpha=-1.0), dict(beta=-1e-9), dict(delta=-0.1),
+    dict(window=0), dict(window=4097), dict(level_rho=(0.0,)), dict(level_rho=(1.5,)),
+    dict(level_bound=(1.0, 0.5), level_lambda=(0.1, 0.2, 0.3), level_rho=(0.8, 0.6, 0.4)),
+])
+def test_bad_parameters_are_refused(bad):
+    prm = dict(K=4, m_min=1, m_max=8, m_init=1, lat=LAT4, eta=1.0, alpha=0.0, beta=0.0,
+               delta=0.1, window=8, level_bound=(), level_lambda=(0.2,), level_rho=(0.5,))
+    prm.update(bad)
+    if len(prm["lat"]) != prm["K"] + 1:
+        prm["lat"] = [0.0] + [100.0 + n for n in range(1, prm["K"] + 1)]
+    if not 1 <= prm["K"] <= sched.MAX_K:
+        with pytest.raises(ValueError):
+            sched.Scheduler(**{k if k != "lat" else "chunk_latency": v for k, v in prm.items()})
+        # the library refuses it too
+        lib = sched.load_sched()
+        p = sched._Params()
+        p.K, p.m_min, p.m_max, p.m_init, p.eta, p.window, p.levels = prm["K"], 1, 8, 1, 1.0, 8, 1
+        p.level_rho[0] = 0.5
+        h = ctypes.c_void_p()
+        assert lib.ts_sched_create(ctypes.byref(p), ctypes.byref(h)) == 1
+        return
+    with pytest.raises(sched.SchedError) as e:
+        sched.Scheduler(**{k if k != "lat" else "chunk_latency": v for k, v in prm.items()})
+    assert e.value.status == 1
+
+
+def test_null_arguments():
+    lib = sched.load_sched()
+    h = ctypes.c_void_p()
+    assert lib.ts_sched_create(None, ctypes.byref(h)) == 1
+    d = sched._Decision()
+    assert lib.ts_sched_step(None, 0, None, None, None, ctypes.byref(d)) == 1
+    s = sched.Scheduler(4, 1, 8, 1, LAT4, 1.0)
+    assert lib.ts_sched_step(s._h, 1, None, None, None, ctypes.byref(d)) == 1
+    assert lib.ts_sched_step(s._h, -1, None, None, None, ctypes.byref(d)) == 1
+    assert lib.ts_sched_step(s._h, 0, None, None, None, None) == 0      # out may be NULL
+    cnt = ctypes.c_int32()
+    assert lib.ts_sched_placement(s._h, None, None, 4, ctypes.byref(cnt)) == 1
+    assert lib.ts_sched_gpus(s._h, None, None, 0, None) == 1
+
+
+def declared(prefix):
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return sorted(set(re.findall(r"\b(%s\w+)\s*\(" % prefix, text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared("ts_sched_")
+    assert names == ["ts_sched_abi_version", "ts_sched_create", "ts_sched_destroy",
+                     "ts_sched_gpus", "ts_sched_placement", "ts_sched_step"]
+    out = subprocess.run(["nm", "-D", "--defined-only", sched.SCHED_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    assert set(names) <= set(re.findall(r"\bT (ts_sched_\w+)", out))
+    m = re.search(r"#define\s+TS_SCHED_ABI_VERSION\s+(\d+)", open(HEADER).read())
+    assert sched.load_sched().ts_sched_abi_version() == int(m.group(1))
+
+
+def test_header_compiles_as_c_and_cxx_and_struct_layout_matches(tmp_path):
+    src = tmp_path / "use.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "ts_sched.h"\n'
+                   'int main(void){printf("%d %d %d %d\\n", (int)sizeof(ts_sched_params),'
+                   ' (int)sizeof(ts_sched_decision), (int)offsetof(ts_sched_params, level_rho),'
+                   ' (int)offsetof(ts_sched_decision, volatility)); return 0;}\n')
+    inc = os.path.dirname(HEADER)
+    subprocess.run(["g++", "-std=c++11", "-Wall", "-Werror", "-fsyntax-only", "-x", "c++", "-I", inc,
+                    str(src)], check=True)
+    exe = tmp_path / "use"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", inc, str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert got == [ctypes.sizeof(sched._Params), ctypes.sizeof(sched._Decision),
+                   sched._Params.level_rho.offset, sched._Decision.volatility.offset]
