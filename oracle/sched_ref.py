@@ -25,7 +25,8 @@ Readings where the paper leaves a choice open:
      to the lower GPU id;
   R3 rebalancing: g_max is the lowest-id GPU of maximum latency; a move (i, j') has
      L = l(n_gmax) and L' = max(l(n_gmax - 1), l(n_j' + 1)), the latencies of the two GPUs it
-     changes; among equal gains the first in (session id, GPU id) order is taken;
+     changes; among equal gains the move to the less-loaded target is taken (the tie rule of
+     assignment), then the lower target id, then the lower session id;
   R4 kappa_i = alpha + beta * (state bytes of s_i);
   R5 N_req counts every active session, placed or not; rho_max is +infinity while an active
      session has no GPU (all GPUs full), so the autoscaler scales out for it;
@@ -122,11 +123,13 @@ class SchedRef:
                     moved[i] = j
                     Lp = max(self.lat[self.load(moved, gmax)], self.lat[self.load(moved, j)])
                     gain = (L - Lp) - self.eta * self.kappa(i)
-                    if best is None or gain > best[0]:
-                        best = (gain, i, j)
+                    tie = (self.load(phi, j), j, i)   # R3: less-loaded target, lower ids
+                    if best is None or gain > best[0] or (gain == best[0] and tie < best[1]):
+                        best = (gain, tie)
             if best is None or not best[0] > 0.0:
                 break
-            phi[best[1]] = best[2]
+            _, (_, j, i) = best
+            phi[i] = j
             stats["migrations"] += 1
 
     def pending(self):

@@ -262,12 +262,12 @@ def pin_closed_loop_trace(mod):
     assert groups(s) == {1: [2, 4]} and d["rho_max"] == 0.5
     # E6: 1, 3, 5 return: 1 and 3 fill g1, 5 is pending (rho_max = inf) -> M_tar = ceil(5/2) = 3:
     # new GPUs g3, g4 (fresh ids); 5 -> g3 (tie with g4 at L = 330, lower id); rebalance from
-    # g1 = {1,2,3,4}: to g3 or g4 L' = 260, gain 70 -> session 1 -> g3 (first target); then from
-    # g1 = {2,3,4}: to g3 L' = 260 (gain 0), to g4 L' = 200 (gain 60) -> session 2 -> g4; then
-    # (2,2,1) stops.
+    # g1 = {1,2,3,4}: to g3 (load 1) or g4 (load 0) L' = 260, gain 70 -> the less-loaded g4 takes
+    # session 1; then from g1 = {2,3,4}: to g3 or g4 (both load 1) L' = 200, gain 60 -> the lower
+    # id, g3, takes session 2; then (2,2,1) stops.
     d = s.step(ev(SR.ACTIVATE, 1, 3, 5))
     assert (d["m"], d["m_target"], d["placed"], d["migrations"], d["pending"]) == (3, 3, 3, 2, 0)
-    assert groups(s) == {1: [3, 4], 3: [1, 5], 4: [2]}
+    assert groups(s) == {1: [3, 4], 3: [2, 5], 4: [1]}
 
 
 def pin_pending_when_full(mod):
@@ -366,6 +366,7 @@ MUTANTS = {
                            "Lp = self.lat[self.load(moved, j)]"),
     "lprime_source_only": ("Lp = max(self.lat[self.load(moved, gmax)], self.lat[self.load(moved, j)])",
                            "Lp = self.lat[self.load(moved, gmax)]"),
+    "rebalance_tie_ignores_load": ("tie = (self.load(phi, j), j, i)", "tie = (j, i)"),
     "gmax_min": ("key=lambda g: (-lat_of[g], g)", "key=lambda g: (lat_of[g], g)"),
     "assign_tie_more_loaded": ("key = (self.bottleneck(trial, gpus), n, g)",
                                "key = (self.bottleneck(trial, gpus), -n, g)"),
