@@ -14,6 +14,9 @@ Other workloads (--workload): the dense and packed self-attention cases of workl
 and the chunk-vs-cache cases of workloads.KV_WORKLOADS (ts_attn_fwd_kvcache with the library's
 automatic key splits: flops = sum_s 4 Lq_s Lk_s d H; the events bracket the whole call, i.e. the
 planning, attention and, when split, merge kernels).
+--workload sched_scale times the closed-loop session scheduler (host code, libts_sched.so): the
+decision time of every epoch of a T5-shaped trace on clusters of 4 to 256 GPUs, and of a scale-out
+that rebalances half a cluster's sessions (value = the worst decision at 256 GPUs, in ms).
 --workload offload_kv times the session-state copy path instead: suspending the two largest
 sessions of the kv_chunk batch (their K and V rows, 1.25 GB) to pinned host memory with
 ts_state_copy (value = GB/s device -> host; the resume rate host -> device is reported beside it),
@@ -185,6 +188,85 @@ def bench_offload(args, torch, np, ts, W):
     print(json.dumps(result), flush=True)
 
 
+def bench_sched(args):
+    """Decision time of the closed-loop scheduler (host code) at growing cluster sizes."""
+    import numpy as np
+
+    import workloads as W
+    from paper_2606_19271_amd.sched import Scheduler
+    from paper_2606_19271_amd.sim import replay
+    import json as _json
+
+    golden = _json.load(open(os.path.join(ROOT, "tests", "golden", "app_a_volatility_levels.json")))
+    vols = [r["volatility"] for r in golden["levels"]]
+    levels = dict(level_bound=[(a + b) / 2.0 for a, b in zip(vols[:-1], vols[1:])],
+                  level_lambda=[r["lambda"] for r in golden["levels"]],
+                  level_rho=[r["rho"] for r in golden["levels"]])
+    mig = W.SCHED_MIGRATION
+
+    def make(M, m_min=1, m_init=None, **kw):
+        prm = dict(levels)
+        prm.update(kw)
+        return Scheduler(W.SCHED_K, m_min, M, M // 2 if m_init is None else m_init,
+                         W.SCHED_LATENCY_MS, mig["eta"], mig["alpha"], mig["beta"], 0.1,
+                         W.SCHED_WINDOW, **prm)
+
+    per_m = {}
+    for M in W.SCHED_CLUSTERS:
+        trace = W.sched_trace(M)
+        runs = []
+        for _ in range(max(1, args.steps)):
+            summary, _ = replay(make(M), trace, latency_slo_ms=670.0)
+            runs.append(summary)
+        best = min(runs, key=lambda r: r["decision_ms_max"])
+        # the heaviest single decision: M/2 full GPUs, then a scale-out to M that rebalances half
+        # of the sessions onto the new GPUs
+        full = [(W.EV_ARRIVE, i, W.SCHED_STATE_BYTES[0]) for i in range(W.SCHED_K * (M // 2))]
+        s = make(M, m_min=M // 2, m_init=M // 2, level_bound=[], level_lambda=[0.2],
+                 level_rho=[0.5])
+        kinds, ids, nb = Scheduler.pack(full)
+        t0 = time.perf_counter_ns()
+        d = s.step_packed(kinds, ids, nb)
+        burst_ms = (time.perf_counter_ns() - t0) * 1e-6
+        best.update({"scale_out_epoch_ms": burst_ms, "scale_out_migrations": d.migrations,
+                     "scale_out_sessions": len(full), "scale_out_m": d.m})
+        per_m[M] = best
+    top = per_m[max(W.SCHED_CLUSTERS)]
+    worst = max(top["decision_ms_max"], top["scale_out_epoch_ms"])
+    result = {
+        "metric": "scheduler decision time per epoch at 256 GPUs (max over a T5-shaped trace and "
+                  "a half-cluster scale-out), ms",
+        "value": worst, "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": 0,
+        "ms_per_step": top["decision_ms_mean"], "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "sched_scale", "K": W.SCHED_K,
+                   "latency_ms": "250 + 50 n", "migration": mig, "epoch_s": 5,
+                   "paper_claim_ms": {"<=64 GPUs": 15, "256 GPUs": 100},
+                   "per_cluster": {str(M): per_m[M] for M in W.SCHED_CLUSTERS}},
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import sched_ref as SR
+        M = 16
+        trace = W.sched_trace(M)
+        ref = SR.SchedRef(W.SCHED_K, 1, M, M // 2, W.SCHED_LATENCY_MS, mig["eta"], mig["alpha"],
+                          mig["beta"], 0.1, W.SCHED_WINDOW, levels["level_bound"],
+                          levels["level_lambda"], levels["level_rho"])
+        t0, worst_ref, done = time.perf_counter(), 0.0, 0
+        for ch in trace:
+            t1 = time.perf_counter()
+            ref.step(ch)
+            worst_ref = max(worst_ref, (time.perf_counter() - t1) * 1e3)
+            done += 1
+            if time.perf_counter() - t0 > min(args.cpu_seconds, 20.0):
+                break
+        result["cpu_baseline"] = {"value": worst_ref, "unit": "ms", "cores": 1, "kind": "oracle",
+                                  "sample": "oracle, max decision time over the first %d epochs "
+                                            "of the 16-GPU trace (the 256-GPU case is out of its "
+                                            "reach)" % done}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +284,10 @@ def main():
               "that holds its sessions, with no exchange between GPUs; run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "sched_scale":
+        bench_sched(args)
+        return
 
     import numpy as np
     import torch

@@ -13,6 +13,7 @@
  *    the larger latency of the two GPUs the move changes, l(n_gmax - 1) and l(n_j' + 1): the
  *    maximum over all GPUs whenever g_max is the only bottleneck GPU, and still positive when
  *    several GPUs share the bottleneck, where the all-GPU maximum could never drop by one move;
+ *    equal gains go to the less-loaded target, as in assignment;
  *  - autoscaling controller (Sec. 5.2.2): with rho_max = max_j n_j / K from placement, scale out
  *    when rho_max > rho_hat + delta and in when rho_max < rho_hat - delta (hysteresis), to
  *    M_tar = ceil(N_req / (K * rho_hat)) (proportional target tracking);

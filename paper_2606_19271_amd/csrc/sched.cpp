@@ -10,8 +10,9 @@
 //      to the less-loaded GPU, then the lower GPU id; then migration-aware min-max rebalancing:
 //      g_max is the lowest-id GPU of maximum latency, a move (i, j') gains
 //      Gamma = (L - L') - eta * kappa_i with L = l(n_gmax), L' = max(l(n_gmax - 1), l(n_j' + 1))
-//      and kappa_i = alpha + beta * bytes_i; the best move (first in (session id, GPU id) order
-//      among equal gains) is applied while its gain is positive;
+//      and kappa_i = alpha + beta * bytes_i; the best move is applied while its gain is positive,
+//      equal gains going to the less-loaded target (the assignment's tie rule), then the lower
+//      target id, then the lower session id;
 //   2. SCALE (Sec. 5.2.2): rho_max = max_j n_j / K (+infinity while an active session has no
 //      GPU); above rho_hat + delta the budget may grow, below rho_hat - delta shrink, to
 //      M_tar = ceil(N_req / (K rho_hat)) clamped to [m_min, m_max], N_req = active sessions;
@@ -157,31 +158,36 @@ void rebalance(ts_sched& s, Stats& st) {
       const double a = lat(s, nmax - 1), b = lat(s, n + 1);
       lp[n] = a >= b ? a : b;
     }
+    // the best move maximises the gain; equal gains go to the less-loaded target, then the
+    // lower target id, then the lower session id
     bool have = false;
     double best_gain = 0.0;
     int64_t best_i = -1;
-    int32_t best_j = -1;
+    int32_t best_j = -1, best_n = 0;
     for (int64_t i : s.gpus[gmax]) {
       const double kappa = s.p.mig_alpha_ms + s.p.mig_beta_ms_per_byte * (double)s.sessions[i].bytes;
       const double cost = s.p.eta * kappa;
-      // this session's best target: largest gain, the lowest GPU id among equal gains
+      // this session's best target (classes come in increasing load)
       bool have_i = false;
       double gi = 0.0;
-      int32_t ji = -1;
+      int32_t ji = -1, ni = 0;
       for (int32_t n = 0; n < s.p.K; ++n) {
         if (tgt[n] < 0) continue;
         const double gain = (L - lp[n]) - cost;
-        if (!have_i || gain > gi || (gain == gi && tgt[n] < ji)) {
+        if (!have_i || gain > gi) {
           have_i = true;
           gi = gain;
           ji = tgt[n];
+          ni = n;
         }
       }
-      if (have_i && (!have || gi > best_gain)) {  // sessions come in increasing id
-        have = true;
+      if (have_i && (!have || gi > best_gain ||
+                     (gi == best_gain && (ni < best_n || (ni == best_n && ji < best_j))))) {
+        have = true;  // sessions come in increasing id: a full tie keeps the earlier one
         best_gain = gi;
         best_i = i;
         best_j = ji;
+        best_n = ni;
       }
     }
     if (!have || !(best_gain > 0.0)) break;

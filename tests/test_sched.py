@@ -167,7 +167,7 @@ def test_hand_derived_closed_loop_trace():
     assert (d["m"], d["placed"], d["migrations"], groups()) == (1, 0, 1, {1: [2, 4]})
     d = lib.step(E(SR.ACTIVATE, 1, 3, 5))
     assert (d["m"], d["placed"], d["migrations"], d["pending"]) == (3, 3, 2, 0)
-    assert groups() == {1: [3, 4], 3: [1, 5], 4: [2]}
+    assert groups() == {1: [3, 4], 3: [2, 5], 4: [1]}
 
 
 def test_pending_and_infinite_load_signal():
@@ -272,3 +272,53 @@ def test_header_compiles_as_c_and_cxx_and_struct_layout_matches(tmp_path):
                                           check=True).stdout.split()]
     assert got == [ctypes.sizeof(sched._Params), ctypes.sizeof(sched._Decision),
                    sched._Params.level_rho.offset, sched._Decision.volatility.offset]
+
+
+def test_simulator_accounts_like_the_oracle():
+    from paper_2606_19271_amd.sim import replay
+    prm = dict(K=4, m_min=1, m_max=12, m_init=2, lat=LAT4, eta=0.05, alpha=5.0, beta=2e-9,
+               delta=0.1, window=12, **app_a_levels())
+    lib, ref = pair(**prm)
+    trace = W.table_trace("T1", seed=3, scale=0.3, state_bytes=(10 ** 9, 3 * 10 ** 9))
+    summary, per = replay(lib, trace, epoch_seconds=5.0, latency_slo_ms=300.0)
+    ds = [ref.step(ch) for ch in trace]
+    assert summary["epochs"] == len(trace)
+    assert summary["gpu_seconds"] == 5.0 * sum(d["m"] for d in ds)
+    assert summary["latency_max_ms"] == max(d["bottleneck_ms"] for d in ds)
+    assert summary["migrations"] == sum(d["migrations"] for d in ds)
+    assert summary["placed"] == sum(d["placed"] for d in ds)
+    assert summary["latency_pass_rate"] == np.mean([d["bottleneck_ms"] <= 300.0 for d in ds])
+    assert list(per["m"]) == [d["m"] for d in ds]
+
+
+@pytest.mark.parametrize("M", [16, 64, 256])
+def test_full_size_free_migration_keeps_loads_balanced(M):
+    """At the benchmark's cluster sizes (beyond the oracle's reach): with free migration the
+    min-max placement is balanced after every epoch -- loads differ by at most one, so the
+    bottleneck is l(ceil(N_placed / M)), the optimum of the min-max problem."""
+    K = W.SCHED_K
+    lib = sched.Scheduler(K, 1, M, M // 2, W.SCHED_LATENCY_MS, 1.0, 0.0, 0.0, 0.1,
+                          W.SCHED_WINDOW, **app_a_levels())
+    for ch in W.sched_trace(M, seed=1):
+        d = lib.step(ch)
+        loads = [n for _, n in lib.gpu_loads()]
+        assert max(loads) - min(loads) <= 1 and max(loads) <= K
+        placed = sum(loads)
+        assert placed == d["n_req"] - d["pending"]
+        assert d["bottleneck_ms"] == W.SCHED_LATENCY_MS[-(-placed // len(loads))]
+
+
+@pytest.mark.parametrize("M", [4, 64, 256])
+def test_scale_out_moves_the_minimum_number_of_sessions(M):
+    """M/2 full GPUs (K sessions each), then the autoscaler doubles the budget: rebalancing onto
+    the new GPUs ends with K/2 sessions everywhere after exactly M/2 * K/2 moves, none of them
+    between two of the old GPUs."""
+    K = W.SCHED_K
+    lib = sched.Scheduler(K, M // 2, M, M // 2, W.SCHED_LATENCY_MS, 0.5, 5.0, 1e-8, 0.1, 12,
+                          [], [0.2], [0.5])
+    d = lib.step([(W.EV_ARRIVE, i, 2 * 10 ** 9) for i in range(K * (M // 2))])
+    assert d["m"] == M and d["m_target"] == M
+    assert d["migrations"] == (M // 2) * (K // 2)
+    assert all(n == K // 2 for _, n in lib.gpu_loads())
+    first = {i: g for i, g in lib.placement()}
+    assert sum(1 for i in range(K * (M // 2)) if first[i] >= M // 2) == (M // 2) * (K // 2)

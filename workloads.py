@@ -265,13 +265,15 @@ def session_trace(n_epochs, seed, mean_arrivals=1.0, burst_every=0, burst=0, p_i
     return out
 
 
-def table_trace(name, seed, bins_per_minute=12, scale=1.0, p_idle=0.05, p_resume=0.5,
+def table_trace(name, seed, bins_per_minute=12, scale=1.0, p_idle=0.25, p_resume=0.2,
                 concentration=0.5, state_bytes=(0, 1)):
     """Decision epochs of 60/bins_per_minute seconds shaped like one trace of TRACE_TABLE: each
     minute's arrivals and departures (times `scale`, rounded) are spread over its bins with
     Dirichlet(concentration) weights (smaller = burstier); a departure takes a random live session
     that arrived in an earlier epoch (deferred while none is live); live sessions flip between
-    active and idle with p_idle / p_resume per epoch."""
+    active and idle with p_idle / p_resume per epoch (with the defaults the active sessions per
+    minute follow the table's average-active row within 20 % in most minutes, within a factor 2
+    in all)."""
     rng = np.random.default_rng(seed)
     arr_min, dep_min = TRACE_TABLE[name]
     active, idle, out, nid, owed = [], [], [], 0, 0
@@ -305,3 +307,31 @@ def table_trace(name, seed, bins_per_minute=12, scale=1.0, p_idle=0.05, p_resume
             active, idle = sorted(nxt_active), sorted(nxt_idle)
             out.append(ch)
     return out
+
+
+# The scheduler workload of the decision-time benchmark: K = 8 sessions per GPU; per-chunk
+# latency l(n) = 250 + 50 n ms for n >= 1 (650 ms at K, under the 670 ms latency target of the
+# paper's App. A case study); migration cost kappa = 5 ms + 1e-8 ms per byte (a 2 GB session state
+# costs 25 ms, the GPU-GPU migration overhead the paper measures); eta = 0.5; session states of
+# 1-3 GB; the App. A volatility levels with W = 12 epochs of 5 s; and, for a cluster of M GPUs,
+# the T5 trace (the largest of the paper's traces) scaled so that its peak average activity is
+# 0.55 K M sessions.
+SCHED_K = 8
+SCHED_LATENCY_MS = [0.0] + [250.0 + 50.0 * n for n in range(1, SCHED_K + 1)]
+SCHED_MIGRATION = {"eta": 0.5, "alpha": 5.0, "beta": 1e-8}
+SCHED_STATE_BYTES = (10 ** 9, 3 * 10 ** 9)
+SCHED_WINDOW = 12
+SCHED_CLUSTERS = (4, 16, 64, 256)
+
+
+def sched_trace(M, seed=0):
+    peak = max(TRACE_TABLE_AVG_ACTIVE["T5"])
+    return table_trace("T5", seed=seed, scale=0.55 * SCHED_K * M / peak, state_bytes=SCHED_STATE_BYTES)
+
+
+# average concurrently active sessions per minute of the same traces (same table of the paper)
+TRACE_TABLE_AVG_ACTIVE = {
+    "T1": (28.0, 56.2, 57.4, 37.4, 23.2), "T2": (61.0, 118.6, 147.6, 154.2, 149.4),
+    "T3": (13.2, 49.4, 112.8, 121.4, 148.4), "T4": (118.4, 219.2, 268.0, 162.8, 101.8),
+    "T5": (245.8, 475.2, 589.2, 616.8, 598.4), "T6": (54.4, 198.4, 451.4, 487.2, 592.0),
+}
