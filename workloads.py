@@ -214,8 +214,8 @@ def sample_rows(w, n_random=64, seed=None):
 # Event codes of one session change; the values are the ones of the scheduler's C ABI.
 EV_ARRIVE, EV_DEPART, EV_ACTIVATE, EV_IDLE = 0, 1, 2, 3
 
-# Per-minute arrivals and departures of the six evaluation traces of the paper (appendix of
-# workload statistics, table of evaluated trace characteristics): T1-T3 ran on the H20 cluster,
+# Per-minute arrivals and departures of the six evaluation traces of the paper (App. B, table
+# of evaluated trace characteristics): T1-T3 ran on the H20 cluster,
 # T4-T6 on the B300 cluster.  The traces themselves are not public; only these aggregates are.
 TRACE_TABLE = {
     "T1": ((122, 130, 66, 22, 18), (44, 86, 88, 64, 38)),
@@ -312,7 +312,7 @@ def table_trace(name, seed, bins_per_minute=12, scale=1.0, p_idle=0.25, p_resume
 # The scheduler workload of the decision-time benchmark: K = 8 sessions per GPU; per-chunk
 # latency l(n) = 250 + 50 n ms for n >= 1 (650 ms at K, under the 670 ms latency target of the
 # paper's App. A case study); migration cost kappa = 5 ms + 1e-8 ms per byte (a 2 GB session state
-# costs 25 ms, the GPU-GPU migration overhead the paper measures); eta = 0.5; session states of
+# costs 25 ms, the GPU-GPU migration overhead the paper measures in Sec. 7.5); eta = 0.5; session states of
 # 1-3 GB; the App. A volatility levels with W = 12 epochs of 5 s; and, for a cluster of M GPUs,
 # the T5 trace (the largest of the paper's traces) scaled so that its peak average activity is
 # 0.55 K M sessions.
