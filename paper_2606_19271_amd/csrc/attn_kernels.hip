@@ -227,15 +227,18 @@ __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const V
 }
 
 // exp2(S*c - m_c) for the 32 scores of the lane, packed to the bf16 B operands of the PV
-// product, with their sum (accumulated from the bf16 values the product will use).
+// product, with their sum, accumulated in fp32 from the bf16 values the product will use (so a
+// row dominated by one key returns that key's value exactly).  Each packed pair is widened by a
+// shift and a mask and summed with plain fp32 adds: v_dot2_f32_bf16 would do it in one
+// instruction, but it issues to the matrix core and measured up to ~7x slower while the other
+// wave of the SIMD streams MFMAs.
 template <bool kMasked>
 __device__ __forceinline__ float exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
                                           float m_c, float c, int keys_valid, int hb) {
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float lsum[kBN / 16];  // independent partial sums, one per 16-key step
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t) {
-    lsum[t] = 0.0f;
+    float pair[4];
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
       float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
@@ -250,8 +253,10 @@ __device__ __forceinline__ float exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&
       bf16x2 pb = __builtin_convertvector(e, bf16x2);
       p[t][m] = pb[0];
       p[t][m + 1] = pb[1];
-      lsum[t] = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum[t], false);
+      const unsigned u = __builtin_bit_cast(unsigned, pb);
+      pair[m >> 1] = __uint_as_float(u << 16) + __uint_as_float(u & 0xffff0000u);
     }
+    lsum[t] = (pair[0] + pair[1]) + (pair[2] + pair[3]);
   }
   float lt = lsum[0];
 #pragma unroll
