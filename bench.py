@@ -216,7 +216,8 @@ def bench_sched(args):
         trace = W.sched_trace(M)
         runs = []
         for _ in range(max(1, args.steps)):
-            summary, _ = replay(make(M), trace, latency_slo_ms=670.0)
+            summary, _ = replay(make(M), trace, latency_slo_ms=670.0,
+                                chunk_latency=W.SCHED_LATENCY_MS)
             runs.append(summary)
         best = min(runs, key=lambda r: r["decision_ms_max"])
         # the heaviest single decision: M/2 full GPUs, then a scale-out to M that rebalances half

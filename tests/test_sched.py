@@ -291,6 +291,29 @@ def test_simulator_accounts_like_the_oracle():
     assert list(per["m"]) == [d["m"] for d in ds]
 
 
+def test_simulator_gap_to_the_minmax_optimum():
+    """The optimum the gap is measured against is the exhaustive min-max placement: checked by
+    brute force on a small cluster; free migration reaches it (gap 0), costly migration does not
+    always."""
+    from paper_2606_19271_amd.sim import replay
+    lat = [0.0, 100.0, 170.0, 250.0]
+    lib = sched.Scheduler(3, 3, 3, 3, lat, 1.0, 0.0, 0.0, 0.1, 4, [], [0.2], [0.5])
+    trace = W.session_trace(80, seed=9, mean_arrivals=0.6, p_idle=0.15, p_resume=0.3, p_depart=0.1)
+    summary, per = replay(lib, trace, chunk_latency=lat)
+    assert summary["gap_to_minmax_optimum_max"] == 0.0
+    ref = SR.SchedRef(3, 3, 3, 3, lat, 1.0, 0.0, 0.0, 0.1, 4, [], [0.2], [0.5])
+    for t, ch in enumerate(trace):
+        d = ref.step(ch)
+        placed = d["n_req"] - d["pending"]
+        best = min(max(lat[assign.count(g)] for g in range(3))
+                   for assign in itertools.product(range(3), repeat=placed)
+                   if max((assign.count(g) for g in range(3)), default=0) <= 3)
+        assert per["optimum_ms"][t] == best
+    costly = sched.Scheduler(3, 3, 3, 3, lat, 1.0, 1000.0, 0.0, 0.1, 4, [], [0.2], [0.5])
+    summary, _ = replay(costly, trace, chunk_latency=lat)
+    assert summary["gap_to_minmax_optimum_mean"] > 0.0
+
+
 @pytest.mark.parametrize("M", [16, 64, 256])
 def test_full_size_free_migration_keeps_loads_balanced(M):
     """At the benchmark's cluster sizes (beyond the oracle's reach): with free migration the
