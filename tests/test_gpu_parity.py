@@ -321,3 +321,50 @@ def test_closed_form_golden_cases():
         assert np.all(np.abs(got - exp) <= 2e-2), c["name"]
         assert np.abs(got - exp).mean() <= 2e-3, c["name"]
         assert np.all(as_f64(o)[:, :, d:] == 0.0)  # zero V channels stay zero
+
+
+# --------------------------------------------------------------------------- the size limit
+
+def test_segments_at_the_byte_limit_sampled():
+    """A segment at the largest size the ABI accepts, (L + 256) * H * d * 2 < 2^31 bytes, in a
+    packed batch whose second segment starts beyond 2 GiB: exercises the 32-bit in-segment
+    offsets at their limit and the 64-bit segment bases (H = 128 keeps the attention cheap)."""
+    H, d = 128, 128
+    row_bytes = H * d * 2
+    L = (1 << 31) // row_bytes - 256 - 1          # 65279: the largest accepted segment
+    seqlens = [L, 40000]
+    T = sum(seqlens)
+    assert (L + 256) * row_bytes < (1 << 31) <= (L + 257) * row_bytes
+    assert L * row_bytes < (1 << 31) < T * row_bytes
+    say("byte limit", "L=%d T=%d H=%d d=%d" % (L, T, H, d))
+    q, k, v = W.make_device_inputs(T, H, d, seed=21, device=torch.device("cuda"))
+    cu_np = np.array([0, L, T], dtype=np.int32)
+    cu = torch.from_numpy(cu_np).cuda()
+    scale = W.Workload("x", (T,), H, d, 0).scale
+    o = ts.ts_attn_fwd_varlen(q, k, v, cu, L, scale=scale)
+    o_dense = ts.ts_attn_fwd(q[:L].view(1, L, H, d), k[:L].view(1, L, H, d), v[:L].view(1, L, H, d),
+                             scale=scale).view(L, H, d)
+    torch.cuda.synchronize()
+    # one past the limit is refused on the host, before any launch
+    with pytest.raises(ts.TsAttnError):
+        ts.ts_attn_fwd_varlen(q[:L + 1], k[:L + 1], v[:L + 1],
+                              torch.tensor([0, L + 1], dtype=torch.int32, device="cuda"), L + 1)
+    rng = np.random.default_rng(5)
+    row_t = np.concatenate([[0, L - 1, L - 2, L - 255, L, T - 1, T - 300],
+                            rng.integers(0, T, 57)]).astype(np.int64)
+    row_h = np.concatenate([[0, H - 1, 77, H - 1, H - 1, H - 1, 3],
+                            rng.integers(0, H, 57)]).astype(np.int32)
+    tt, hh = torch.from_numpy(row_t).cuda(), torch.from_numpy(row_h).long().cuda()
+    got = o[tt, hh].cpu()
+    i0 = torch.from_numpy(np.nonzero(row_t < L)[0])  # rows of the first segment: dense == packed
+    assert torch.equal(o_dense[tt[i0.cuda()], hh[i0.cuda()]].cpu(), got[i0])
+    del o, o_dense
+    hq, hk, hv = (W.bf16_bits(x.cpu()) for x in (q, k, v))
+    del q, k, v
+    torch.cuda.empty_cache()
+    say("oracle rows", row_t.size)
+    ref = ts_ref.attn_rows(hq, hk, hv, cu_np, scale, row_t, row_h)
+    e = assert_parity(as_f64(got), ref, "byte limit")
+    trivial = errors(np.zeros_like(ref), ref)
+    say("byte limit errors", e, "zero-output errors", trivial)
+    assert e["mean_abs"] < 0.1 * trivial["mean_abs"]

@@ -335,3 +335,18 @@ TRACE_TABLE_AVG_ACTIVE = {
     "T3": (13.2, 49.4, 112.8, 121.4, 148.4), "T4": (118.4, 219.2, 268.0, 162.8, 101.8),
     "T5": (245.8, 475.2, 589.2, 616.8, 598.4), "T6": (54.4, 198.4, 451.4, 487.2, 592.0),
 }
+
+
+def make_device_inputs(T, H, d, seed, device):
+    """q, k, v [T, H, d] bf16 drawn N(0, 1) directly on `device` from a torch generator seeded
+    with `seed` (float32 draws in the order q, k, v, rounded once to bf16): for tensors of
+    several GB, where drawing on the host would take minutes.  Host copies of the same tensors
+    serve the oracle."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    out = []
+    for _ in range(3):
+        x = torch.randn((T, H, d), generator=g, device=device, dtype=torch.float32)
+        out.append(x.to(torch.bfloat16))
+        del x
+    return tuple(out)
