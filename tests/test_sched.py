@@ -345,3 +345,33 @@ def test_scale_out_moves_the_minimum_number_of_sessions(M):
     assert all(n == K // 2 for _, n in lib.gpu_loads())
     first = {i: g for i, g in lib.placement()}
     assert sum(1 for i in range(K * (M // 2)) if first[i] >= M // 2) == (M // 2) * (K // 2)
+
+
+def test_random_valid_and_invalid_batches_match_the_oracle():
+    """Batches of random changes, many of them invalid (unknown ids, repeated arrivals,
+    activations of active sessions...): the library refuses exactly the batches the oracle
+    refuses, with nothing changed, and agrees on everything else."""
+    prm = dict(K=3, m_min=0, m_max=5, m_init=1, lat=[0.0, 100.0, 160.0, 250.0], eta=0.5,
+               alpha=10.0, beta=1e-3, delta=0.1, window=4, level_bound=(0.7,),
+               level_lambda=(0.1, 0.3), level_rho=(0.9, 0.5))
+    lib, ref = pair(**prm)
+    rng = np.random.default_rng(17)
+    refused = 0
+    for t in range(400):
+        ch = [(int(rng.integers(0, 5)) if rng.random() < 0.03 else int(rng.integers(0, 4)),
+               int(rng.integers(0, 24)), int(rng.integers(-1, 5000)) if rng.random() < 0.05
+               else int(rng.integers(0, 5000)))
+              for _ in range(int(rng.integers(0, 5)))]
+        try:
+            b = ref.step(ch)
+        except SR.SchedError:
+            b = None
+        if b is None:
+            refused += 1
+            with pytest.raises(sched.SchedError):
+                lib.step(ch)
+        else:
+            a = lib.step(ch)
+            assert same_decision(a, b), (t, a, b)
+        assert lib.placement() == ref.placement() and lib.gpu_loads() == ref.gpu_loads(), t
+    assert 50 < refused < 350
