@@ -8,8 +8,8 @@
 // sessions leave are all lists of range copies: dst[d, d + n) = src[s, s + n).
 //
 // Design: one launch copies up to kMaxRanges ranges, passed by value in the kernel arguments
-// (no device allocation, no host-to-device upload).  Every range is cut into 16 KiB chunks; one
-// 256-thread workgroup copies one chunk with 16-byte accesses, four loads in flight per thread
+// (no device allocation, no host-to-device upload).  Every range is cut into 32 KiB chunks; one
+// 256-thread workgroup copies one chunk with 16-byte accesses, eight loads in flight per thread
 // before the stores, so a host-memory side keeps many PCIe requests outstanding.  The chunk
 // index space is dense: a prefix over the ranges' chunk counts maps a workgroup to its range.
 // Pinned host memory is reached directly at its (unified) virtual address; the side that lives
@@ -22,8 +22,8 @@
 namespace tsstate {
 
 constexpr int kThreads = 256;
-constexpr int kPerThread = 4;                      // 16-byte vectors per thread per chunk
-constexpr int64_t kChunk = kThreads * kPerThread * 16;  // 16 KiB
+constexpr int kPerThread = 8;                      // 16-byte vectors per thread per chunk
+constexpr int64_t kChunk = kThreads * kPerThread * 16;  // 32 KiB
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
