@@ -368,3 +368,20 @@ def test_segments_at_the_byte_limit_sampled():
     trivial = errors(np.zeros_like(ref), ref)
     say("byte limit errors", e, "zero-output errors", trivial)
     assert e["mean_abs"] < 0.1 * trivial["mean_abs"]
+
+
+def test_head_dim_64_long_segments_sampled():
+    """d = 64 over long segments (hundreds of key tiles, the XCD remap of a large grid, the
+    per-channel K offsets of the DiT workloads), sampled rows against the oracle."""
+    w = W.Workload("d64_long", (20000, 7777), 6, 64, 64, k_offset=True)
+    say("d64 long", w.seqlens, w.H, w.d)
+    q, k, v = W.make_inputs(w)
+    cu = torch.tensor(w.cu_seqlens, device="cuda")
+    o = ts.ts_attn_fwd_varlen(q.cuda(), k.cuda(), v.cuda(), cu, w.max_seqlen)
+    torch.cuda.synchronize()
+    row_t, row_h = W.sample_rows(w)
+    got = o[torch.from_numpy(row_t).cuda(), torch.from_numpy(row_h).long().cuda()].cpu()
+    ref = ts_ref.attn_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), w.cu_seqlens,
+                           w.scale, row_t, row_h)
+    e = assert_parity(as_f64(got), ref, "d64 long")
+    assert e["mean_abs"] < 0.1 * errors(np.zeros_like(ref), ref)["mean_abs"]
