@@ -10,6 +10,8 @@ Prints one JSON line:
                 kernel source (null when the kernel source changed since)
   cpu_baseline  the fp64 oracle timed on this host's cores on a bounded row sample of the same
                 workload, in the same unit; the sampled rows also serve as a parity check
+  config.gemm_bf16_reference  context: torch.matmul's bf16 rate on a 16384^3 product, same device
+                and run (the sustainable MFMA rate at this device's power cap), and value over it
 Other workloads (--workload): the dense and packed self-attention cases of workloads.WORKLOADS,
 and the chunk-vs-cache cases of workloads.KV_WORKLOADS (ts_attn_fwd_kvcache with the library's
 automatic key splits: flops = sum_s 4 Lq_s Lk_s d H; the events bracket the whole call, i.e. the
@@ -101,6 +103,25 @@ def cpu_baseline(w, q, k, v, o_gpu, seconds):
         "sample": "%d (token, head) rows of %s (%.3g fp64 GFLOP of the %.3g GFLOP call), %.1f s"
                   % (done, w.name, flops / 1e9, w.flops / 1e9, t_total),
     }, {"rows": int(done), "max_abs": float(err.max()), "mean_abs": float(err.mean())}
+
+
+def gemm_reference(torch, dev, n=16384, reps=4):
+    """Context only: the bf16 rate of a plain n^3 matrix product by torch.matmul (hipBLASLt)
+    on the same device and run, timed after the attention.  MI355X runs these MFMA-bound loads
+    at a power-capped clock, so this rate, not the nominal peak, is what the device sustains."""
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b, c
+    return {"n": n, "ms": ms, "tflops": 2.0 * n ** 3 / (ms * 1e-3) / 1e12}
 
 
 PCIE5_X16_GBS = 64.0  # one direction, 32 GT/s x 16 lanes
@@ -276,6 +297,8 @@ def main():
     ap.add_argument("--workload", default="dit_large")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-reference", action="store_true",
+                    help="skip the context timing of a plain bf16 matrix product")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of attention, time a plain device copy of this many bytes "
                          "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known traffic)")
@@ -356,6 +379,7 @@ def main():
     kernel_ms = float(np.mean(launch_ms))
     achieved = w.flops / (kernel_ms * 1e-3) / 1e12
     traffic = traffic_bytes(w.name)
+    gemm = None if args.no_gemm_reference else gemm_reference(torch, dev)
 
     result = {
         "metric": METRIC,
@@ -377,7 +401,9 @@ def main():
                    "causal": False, "flops_per_call": w.flops, "hbm_bytes_per_call": w.hbm_bytes,
                    "kernel_ms_mean": kernel_ms, "kernel_ms_min": float(np.min(launch_ms)),
                    "kernel_ms_max": float(np.max(launch_ms)),
-                   "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS},
+                   "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
+                   **({"gemm_bf16_reference": gemm,
+                       "value_over_gemm": value / gemm["tflops"]} if gemm else {})},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic},
     }
