@@ -385,3 +385,20 @@ def test_head_dim_64_long_segments_sampled():
                            w.scale, row_t, row_h)
     e = assert_parity(as_f64(got), ref, "d64 long")
     assert e["mean_abs"] < 0.1 * errors(np.zeros_like(ref), ref)["mean_abs"]
+
+
+def test_q_k_v_may_be_one_tensor():
+    """The ABI lets q, k and v alias one another (only o must be separate): self-similarity
+    attention with q = k = v, packed and dense, against the oracle on the same array."""
+    seqlens = [700, 129]
+    w, q, _, _ = draw(seqlens, 2, 128, seed=91)
+    say("aliased q = k = v")
+    x = q.cuda()
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32), device="cuda")
+    o = ts.ts_attn_fwd_varlen(x, x, x, cu, max(seqlens))
+    o_dense = ts.ts_attn_fwd(x[:700].view(1, 700, 2, 128), x[:700].view(1, 700, 2, 128),
+                             x[:700].view(1, 700, 2, 128)).view(700, 2, 128)
+    torch.cuda.synchronize()
+    ref = oracle_full(q, q, q, seqlens, w.scale)
+    assert_parity(as_f64(o.cpu()), ref, "aliased")
+    assert torch.equal(o_dense.cpu(), o[:700].cpu())
