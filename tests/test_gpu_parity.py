@@ -304,6 +304,49 @@ def test_runs_on_a_side_stream():
     assert_parity(as_f64(o.cpu()), ref, "side stream")
 
 
+def test_concurrent_calls_from_threads_on_separate_streams():
+    """Four host threads, each on its own stream, call the packed attention (split and unsplit
+    chunk calls included) 10 times each; every result equals the single-threaded one bitwise."""
+    import threading
+    seqlens = [700, 0, 333]
+    w, q, k, v = draw(seqlens, 4, 128, seed=67)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    cu = torch.tensor(w.cu_seqlens, device="cuda")
+    ref_o = ts.ts_attn_fwd_varlen(qd, kd, vd, cu, w.max_seqlen)
+    ref_kv, ref_lse = ts.ts_attn_fwd_kvcache(qd, kd, vd, cu, cu, w.max_seqlen, w.max_seqlen,
+                                            return_lse=True, num_splits=3)
+    torch.cuda.synchronize()
+    say("threads")
+    errors_seen = []
+
+    def worker(n):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                for _ in range(10):
+                    if n % 2:
+                        o = ts.ts_attn_fwd_varlen(qd, kd, vd, cu, w.max_seqlen)
+                        lse = None
+                    else:
+                        o, lse = ts.ts_attn_fwd_kvcache(qd, kd, vd, cu, cu, w.max_seqlen, w.max_seqlen,
+                                                        return_lse=True, num_splits=3)
+                    st.synchronize()
+                    if not torch.equal(o, ref_o if n % 2 else ref_kv):
+                        errors_seen.append("output of thread %d" % n)
+                    if lse is not None and not torch.equal(lse, ref_lse):
+                        errors_seen.append("lse of thread %d" % n)
+        except Exception as e:  # reported below
+            errors_seen.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(n,)) for n in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors_seen, errors_seen[:3]
+
+
 # ------------------------------------------------------------------------- closed-form fixtures
 
 def test_closed_form_golden_cases():
