@@ -104,6 +104,36 @@ def test_kv_forced_splits_full(splits, d):
     assert float((o.float() - o1.float()).abs().max()) <= 2e-2
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_kv_random_batches_full(seed):
+    # seeded random chunk batches: per segment a query count and a key count drawn independently
+    # (either may be zero or sit on a tile edge), random heads, head dim, scale and split count
+    # (0 = the library's choice), with and without a per-channel offset on K (which shifts the
+    # scores and so the running maximum)
+    rng = np.random.default_rng(5200 + seed)
+    edge = [0, 1, 63, 64, 65, 255, 256, 257]
+    nseq = int(rng.integers(1, 8))
+    lq = [int(rng.choice(edge)) if rng.random() < 0.4 else int(rng.integers(1, 600)) for _ in range(nseq)]
+    lk = [int(rng.choice(edge)) if rng.random() < 0.4 else int(rng.integers(1, 2000)) for _ in range(nseq)]
+    if sum(lq) == 0:
+        lq[0] = 1
+    if sum(lk) == 0:
+        lk[0] = 1
+    H = int(rng.choice([1, 2, 4]))
+    d = int(rng.choice([64, 128]))
+    scale = None if rng.random() < 0.5 else float(np.float32(rng.uniform(-1.0, 1.5)))
+    splits = int(rng.choice([0, 0, 1, 2, 5]))
+    k_offset = bool(rng.random() < 0.5)
+    w, q, k, v = draw(lq, lk, H, d, 5300 + seed, k_offset=k_offset)
+    sc = w.scale if scale is None else scale
+    what = "kv random seed=%d lq=%r lk=%r H=%d d=%d scale=%r splits=%d" % (seed, lq, lk, H, d, scale, splits)
+    say(what)
+    o, lse = run_kv(w, q, k, v, splits=splits, scale=scale)
+    ro, rlse = oracle(w, q, k, v, sc)
+    assert_parity(as_f64(o), ro, what)
+    check_lse(lse, rlse, what)
+
+
 def test_kv_equal_offsets_is_varlen_bitwise():
     lens = [300, 0, 1000, 65, 1]
     w, q, k, v = draw(lens, lens, 2, 128, 51)

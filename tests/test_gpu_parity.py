@@ -109,6 +109,36 @@ def test_varlen_with_empty_and_tiny_segments_full(d):
     assert_parity(as_f64(o), ref, "varlen d=%d" % d)
 
 
+# lengths at and around the 64-key and 256-query tile edges, mixed with arbitrary ones
+EDGE_LENGTHS = [0, 1, 2, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513]
+
+
+def random_case(rng, max_len=1400):
+    nseq = int(rng.integers(1, 10))
+    lens = [int(rng.choice(EDGE_LENGTHS)) if rng.random() < 0.5 else int(rng.integers(1, max_len))
+            for _ in range(nseq)]
+    if sum(lens) == 0:
+        lens[int(rng.integers(0, nseq))] = int(rng.integers(1, max_len))
+    H = int(rng.choice([1, 2, 3, 5]))
+    d = int(rng.choice([64, 128]))
+    scale = None if rng.random() < 0.5 else float(np.float32(rng.uniform(-1.0, 1.5)))
+    return lens, H, d, scale
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_random_packed_batches_full(seed):
+    # seeded random batches: segment count, lengths, heads, head dim and scale all drawn, so that
+    # tile edges, empty segments and the planner's ordering meet in combinations no listed case has
+    rng = np.random.default_rng(4200 + seed)
+    lens, H, d, scale = random_case(rng)
+    w, q, k, v = draw(lens, H, d, seed=4300 + seed)
+    sc = w.scale if scale is None else scale
+    say("random packed", seed, lens, H, d, scale)
+    ref = oracle_full(q, k, v, lens, sc)
+    o = run_varlen(q, k, v, lens, scale=scale)
+    assert_parity(as_f64(o), ref, "random packed seed=%d %r H=%d d=%d scale=%r" % (seed, lens, H, d, scale))
+
+
 def test_many_segments_beyond_sort_limit():
     rng = np.random.default_rng(9)
     seqlens = rng.integers(0, 6, size=5000).tolist()  # more segments than the plan sorts
