@@ -61,6 +61,17 @@ def test_header_compiles_as_c_and_cxx(tmp_path):
                     "-I", os.path.dirname(HEADER), str(src)], check=True)
 
 
+def test_plain_c_client_builds_and_links(tmp_path):
+    # the C client of tests/c_abi (HIP runtime + this header, -Werror) compiles and links against
+    # the built library; it runs on the GPU in test_gpu_c_abi.py
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("c_abi_build", os.path.join(ROOT, "tests", "c_abi", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    exe = mod.build(str(tmp_path / "caller"))
+    assert os.access(exe, os.X_OK)
+
+
 def test_status_strings(lib):
     for code, name in enumerate(_lib.STATUS_NAMES):
         assert ts.status_str(code).startswith(name)
