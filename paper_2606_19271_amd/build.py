@@ -9,7 +9,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libts_attn.so")
 SOURCES = [os.path.join(CSRC, "attn_kernels.hip"), os.path.join(CSRC, "state_copy.hip"),
-           os.path.join(CSRC, "ts_attn.cpp")]
+           os.path.join(CSRC, "attn_plan.cpp"), os.path.join(CSRC, "ts_attn.cpp")]
 
 SCHED_LIB = os.path.join(HERE, "libts_sched.so")
 SCHED_SOURCES = [os.path.join(CSRC, "sched.cpp")]

@@ -55,7 +55,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) void lds_void;
 
 
-constexpr int kBM = 256;       // queries per work item
+constexpr int kBM = kQueryTile;  // queries per work item
 constexpr int kBN = 64;        // keys per K/V tile
 constexpr int kWaves = 8;      // waves per workgroup, 32 queries each
 constexpr int kThreads = kWaves * 64;
@@ -687,8 +687,6 @@ attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
 // (O_i, lse_i) over disjoint key ranges, O = sum_i exp(lse_i - lse) O_i with
 // lse = log sum_i exp(lse_i) -- a softmax-weighted average over the union of the ranges.  One
 // thread per 8 channels of a row; rows = Tq * H.
-constexpr int kMergeThreads = 256;
-
 template <int D>
 __global__ void __launch_bounds__(kMergeThreads)
 attn_merge_kernel(const float* __restrict__ part_o, const float* __restrict__ part_lse,
@@ -840,19 +838,6 @@ static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
                      a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse);
   return hipGetLastError();
 }
-
-int64_t packed_grid_bound(int32_t total_q, int32_t nseq, int32_t H, int32_t n_split) {
-  // sum_s ceil(Lq_s / BM) <= ceil(Tq / BM) + nseq
-  return (int64_t)H * n_split * (((int64_t)total_q + kBM - 1) / kBM + nseq);
-}
-
-int64_t merge_blocks(int32_t total_q, int32_t H, int32_t d) {
-  return ((int64_t)total_q * H * (d / 8) + kMergeThreads - 1) / kMergeThreads;
-}
-
-int64_t plan_ints(int32_t nseq) { return 2 + 2 * (int64_t)nseq; }
-
-int query_tile() { return kBM; }
 
 hipError_t configure_kernels() {
   hipError_t e;

@@ -1,7 +1,7 @@
 // attn_launch.h -- internal interface between the C ABI layer (ts_attn.cpp) and the kernels
 // (attn_kernels.hip).  Not installed; the public interface is include/ts_attn.h.
 #pragma once
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
 namespace tsattn {
@@ -36,14 +36,17 @@ struct PackedArgs {
   float* part_lse;       // device [n_split][total_q][H] (n_split > 1)
 };
 
+// Sizes shared by the kernels and the host-side planning (attn_plan.cpp).
+constexpr int kQueryTile = 256;             // queries per work item of the attention kernels
+constexpr int kMergeThreads = 256;          // threads per workgroup of the merge kernel
+constexpr int64_t kCopyChunkBytes = 32768;  // bytes copied by one state-copy workgroup
+
 // Upper bound of the number of work items of a packed batch (its launch grid).
 int64_t packed_grid_bound(int32_t total_q, int32_t nseq, int32_t H, int32_t n_split);
 // Workgroups of the merge kernel of a split call.
 int64_t merge_blocks(int32_t total_q, int32_t H, int32_t d);
 // int32 entries of the plan buffer for nseq segments.
 int64_t plan_ints(int32_t nseq);
-// Queries per work item.
-int query_tile();
 
 // Up to kMaxCopyRanges byte-range copies of one state-copy launch (passed by value as a kernel
 // argument): range r copies bytes[r] bytes from src + src[r] to dst + dst[r]; first_chunk is the

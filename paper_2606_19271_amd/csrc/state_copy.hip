@@ -24,6 +24,7 @@ namespace tsstate {
 constexpr int kThreads = 256;
 constexpr int kPerThread = 8;                      // 16-byte vectors per thread per chunk
 constexpr int64_t kChunk = kThreads * kPerThread * 16;  // 32 KiB
+static_assert(kChunk == tsattn::kCopyChunkBytes, "chunk size shared with the host planning");
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
@@ -61,8 +62,6 @@ state_copy_kernel(const char* __restrict__ src, char* __restrict__ dst, tsattn::
 }  // namespace tsstate
 
 namespace tsattn {
-
-int64_t copy_chunk_bytes() { return tsstate::kChunk; }
 
 hipError_t launch_state_copy(const void* src, void* dst, const CopyList& list, bool src_host,
                              bool dst_host, hipStream_t st) {

@@ -2,7 +2,7 @@
 // per-device set-up, the plan buffer of packed batches, and the launches.
 #include "ts_attn.h"
 
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -86,8 +86,10 @@ int check_common(const void* q, const void* k, const void* v, const void* o, int
   if (!isfinite(scale)) return TS_ERR_SCALE;
   if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return TS_ERR_ALIGN;
   const int64_t row_bytes = (int64_t)H * d * 2;
-  if ((longest + 256) * row_bytes >= kByteLimit) return TS_ERR_SHAPE;
-  if (tokens > (int64_t)1 << 31 || tokens * row_bytes / row_bytes != tokens) return TS_ERR_SHAPE;
+  // (longest + 256) * row_bytes < kByteLimit, written so that nothing overflows for any H; it
+  // also bounds row_bytes below 2^23, so tokens * row_bytes fits easily
+  if (longest + 256 > (kByteLimit - 1) / row_bytes) return TS_ERR_SHAPE;
+  if (tokens > (int64_t)1 << 31) return TS_ERR_SHAPE;
   const int64_t bytes = tokens * row_bytes;
   if (overlaps(o, q, bytes) || overlaps(o, k, bytes) || overlaps(o, v, bytes)) return TS_ERR_ALIAS;
   return TS_OK;
@@ -110,8 +112,8 @@ int check_kv(const void* q, const void* k, const void* v, const void* o, const f
   if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return TS_ERR_ALIGN;
   if (((uintptr_t)lse & 3u) != 0) return TS_ERR_ALIGN;
   const int64_t row_bytes = (int64_t)H * d * 2;
-  if ((max_q + 256) * row_bytes >= kByteLimit || (max_k + 256) * row_bytes >= kByteLimit)
-    return TS_ERR_SHAPE;
+  if (max_q + 256 > (kByteLimit - 1) / row_bytes || max_k + 256 > (kByteLimit - 1) / row_bytes)
+    return TS_ERR_SHAPE;  // as in check_common, without overflow for any H
   if (tq > (int64_t)1 << 31 || tk > (int64_t)1 << 31) return TS_ERR_SHAPE;
   const int64_t qb = tq * row_bytes, kb = tk * row_bytes;
   if (ranges_overlap(o, qb, q, qb) || ranges_overlap(o, qb, k, kb) || ranges_overlap(o, qb, v, kb))
@@ -309,7 +311,8 @@ int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_byt
       list.src[i] = e[0];
       list.dst[i] = e[1];
       list.bytes[i] = e[2];
-      list.first_chunk[i + 1] = list.first_chunk[i] + (e[2] + chunk - 1) / chunk;
+      // ceil(bytes / chunk) without forming bytes + chunk - 1 (bytes may be near INT64_MAX)
+      list.first_chunk[i + 1] = list.first_chunk[i] + e[2] / chunk + (e[2] % chunk != 0);
     }
     if (list.first_chunk[list.n] >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
     if (tsattn::launch_state_copy(s_dev, (void*)d_dev, list, s_host, d_host, (hipStream_t)stream) !=
