@@ -109,6 +109,12 @@ def test_dense_argument_checks(lib):
     assert fwd(lib, o=A) == _lib.TS_ERR_ALIAS                      # o == q
     assert fwd(lib, v=BIG + 4096, o=BIG) == _lib.TS_ERR_ALIAS      # o overlaps v
     assert fwd(lib, L=300000, H=40) == _lib.TS_ERR_SHAPE           # beyond the byte limit
+    # head counts whose row size alone passes the byte limit (the check must not overflow)
+    for H in (1 << 23, (1 << 31) - 1):
+        assert fwd(lib, H=H) == _lib.TS_ERR_SHAPE
+        assert fwd(lib, H=H, L=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
+        assert varlen(lib, H=H, max_seqlen=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
+        assert kvcache(lib, H=H, max_k=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
     # empty problems are no-ops that never touch the device
     assert fwd(lib, B=0) == _lib.TS_OK
     assert fwd(lib, L=0) == _lib.TS_OK
