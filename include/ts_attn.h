@@ -36,6 +36,12 @@
  *    in the arithmetic, fixed reduction order), and a row's result does not depend on the
  *    other segments of the batch.
  *  - Thread safety: all entry points may be called concurrently from several host threads.
+ *  - Graph capture: ts_attn_fwd only enqueues kernels, so a call on a capturing stream is
+ *    recorded into the HIP graph and replays with the pointers and sizes it was made with.
+ *    ts_attn_fwd_varlen, ts_attn_fwd_kvcache and ts_state_copy return TS_ERR_CAPTURE on a
+ *    capturing stream: the first two take their plan buffer from a stream-ordered memory pool,
+ *    and the copy looks up where its operands live.  So does any call that would be the first
+ *    on its device, since the one-time device set-up must run outside capture.
  *  - Size limits: (L or max_seqlen + 256) * H * d * 2 bytes must stay below 2^31, and the
  *    work items (H * ceil(L / 256) per sequence; H * (ceil(T / 256) + nseq) for packed
  *    batches; 16 * H * (ceil(total_q / 256) + nseq) for chunk-vs-cache calls) below 2^23.
@@ -50,7 +56,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 3
+#define TS_ATTN_ABI_VERSION 4
 
 typedef enum ts_status {
   TS_OK = 0,
@@ -64,7 +70,8 @@ typedef enum ts_status {
   TS_ERR_HIP = 8,         /* a HIP runtime call or kernel launch failed */
   TS_ERR_NOMEM = 9,       /* device scratch allocation failed */
   TS_ERR_SEGMENTS = 10,   /* cu_seqlens contents invalid (reported only in validation mode) */
-  TS_ERR_MEMORY = 11      /* a copy operand is neither current-device memory nor pinned host memory */
+  TS_ERR_MEMORY = 11,     /* a copy operand is neither current-device memory nor pinned host memory */
+  TS_ERR_CAPTURE = 12     /* the call cannot be recorded into a HIP graph (see "Graph capture") */
 } ts_status;
 
 /*

@@ -7,7 +7,7 @@ from .build import LIB
 TS_OK = 0
 STATUS_NAMES = ["TS_OK", "TS_ERR_NULL", "TS_ERR_SHAPE", "TS_ERR_HEAD_DIM", "TS_ERR_SCALE",
                 "TS_ERR_ALIGN", "TS_ERR_ALIAS", "TS_ERR_UNSUPPORTED", "TS_ERR_HIP",
-                "TS_ERR_NOMEM", "TS_ERR_SEGMENTS", "TS_ERR_MEMORY"]
+                "TS_ERR_NOMEM", "TS_ERR_SEGMENTS", "TS_ERR_MEMORY", "TS_ERR_CAPTURE"]
 globals().update({name: i for i, name in enumerate(STATUS_NAMES)})
 
 _lib = None

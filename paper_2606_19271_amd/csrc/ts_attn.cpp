@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 
 #include "attn_launch.h"
@@ -21,6 +22,7 @@ constexpr int32_t kMaxSplits = 16;                 // key ranges per query tile 
 
 struct DeviceState {
   std::once_flag once;
+  std::atomic<bool> set_up{false};  // init_device has run (whatever its outcome)
   int status = TS_ERR_UNSUPPORTED;  // TS_OK once the device is known to be usable
   int xcd_chunk = 32;
   int cus = 256;
@@ -51,15 +53,34 @@ void init_device(int dev, DeviceState* st) {
   st->status = TS_OK;
 }
 
-// The calling thread's current device, initialised once.
-DeviceState* current_device(int* status) {
+// Whether stream s is recording a HIP graph.  A failed query (which leaves an error behind that
+// a later launch check would report) is cleared and read as "not capturing".
+bool capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return cs != hipStreamCaptureStatusNone;
+}
+
+// The calling thread's current device, initialised once -- never under stream capture, where
+// the set-up's pool creation and kernel attributes have no place (TS_ERR_CAPTURE).
+DeviceState* current_device(int* status, hipStream_t s) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     *status = TS_ERR_UNSUPPORTED;
     return nullptr;
   }
   DeviceState* st = &g_dev[dev];
-  std::call_once(st->once, init_device, dev, st);
+  if (!st->set_up.load(std::memory_order_acquire) && capturing(s)) {
+    *status = TS_ERR_CAPTURE;
+    return nullptr;
+  }
+  std::call_once(st->once, [dev, st] {
+    init_device(dev, st);
+    st->set_up.store(true, std::memory_order_release);
+  });
   *status = st->status;
   return st->status == TS_OK ? st : nullptr;
 }
@@ -222,6 +243,7 @@ const char* ts_attn_status_str(int status) {
     case TS_ERR_NOMEM: return "TS_ERR_NOMEM: device scratch allocation failed";
     case TS_ERR_SEGMENTS: return "TS_ERR_SEGMENTS: invalid cu_seqlens contents";
     case TS_ERR_MEMORY: return "TS_ERR_MEMORY: pointer is neither device memory of the current device nor pinned host memory";
+    case TS_ERR_CAPTURE: return "TS_ERR_CAPTURE: this call cannot be recorded into a HIP graph (packed and copy calls, or a device's first call)";
     default: return "unknown ts_status";
   }
 }
@@ -233,7 +255,7 @@ int ts_attn_fwd(const void* q, const void* k, const void* v, void* o, int32_t B,
   if (rc != TS_OK) return rc;
   if ((int64_t)B * H * ((L + 255) / 256) >= kGridLimit) return TS_ERR_SHAPE;
   if (B == 0 || L == 0) return TS_OK;
-  DeviceState* st = current_device(&rc);
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   tsattn::DenseArgs a{q, k, v, o, B, L, H, d, scale, st->xcd_chunk};
   return tsattn::launch_dense(a, (hipStream_t)stream) == hipSuccess ? TS_OK : TS_ERR_HIP;
@@ -248,7 +270,8 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
   if (rc != TS_OK) return rc;
   if (tsattn::packed_grid_bound(total_tokens, nseq, H, 1) >= kGridLimit) return TS_ERR_SHAPE;
   if (nseq == 0 || total_tokens == 0) return TS_OK;
-  DeviceState* st = current_device(&rc);
+  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   tsattn::PackedArgs a{q, k, v, o, nullptr, cu_seqlens, cu_seqlens, nseq, max_seqlen, max_seqlen,
                        total_tokens, total_tokens, H, d, 1, scale, st->xcd_chunk,
@@ -268,7 +291,8 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
   if (tsattn::packed_grid_bound(total_q, nseq, H, kMaxSplits) >= kGridLimit) return TS_ERR_SHAPE;
   if (tsattn::merge_blocks(total_q, H, d) >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
   if (nseq == 0 || total_q == 0) return TS_OK;
-  DeviceState* st = current_device(&rc);
+  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H);
   tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
@@ -291,8 +315,9 @@ int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_byt
     if (so > src_bytes || n > src_bytes - so || d_o > dst_bytes || n > dst_bytes - d_o)
       return TS_ERR_SHAPE;
   }
+  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // operand lookups are not stream work
   int rc = TS_OK;
-  DeviceState* st = current_device(&rc);
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return TS_ERR_HIP;

@@ -20,7 +20,7 @@ namespace {
 int g_fail = 0;
 int64_t g_calls = 0;
 
-bool known_status(int s) { return s >= TS_OK && s <= TS_ERR_MEMORY; }
+bool known_status(int s) { return s >= TS_OK && s <= TS_ERR_CAPTURE; }
 
 void expect(bool cond, const char* what, long long a, long long b, long long c) {
   if (!cond) {
@@ -121,7 +121,7 @@ int main() {
   expect(ts_state_copy(q, 64, o, 64, nullptr, 1, nullptr) == TS_ERR_NULL, "null ranges", 0, 0, 0);
   expect(ts_state_copy(q, 64, o, 64, nullptr, 0, nullptr) == TS_OK, "no ranges", 0, 0, 0);
 
-  for (int s = -2; s <= TS_ERR_MEMORY + 2; ++s) expect(ts_attn_status_str(s) != nullptr, "status string", s, 0, 0);
+  for (int s = -2; s <= TS_ERR_CAPTURE + 2; ++s) expect(ts_attn_status_str(s) != nullptr, "status string", s, 0, 0);
   std::printf("calls %lld, failures %d\n", (long long)g_calls, g_fail);
   return g_fail == 0 ? 0 : 1;
 }
