@@ -15,13 +15,15 @@ SCHED_LIB = os.path.join(HERE, "libts_sched.so")
 SCHED_SOURCES = [os.path.join(CSRC, "sched.cpp")]
 # no contraction into fused multiply-adds: the scheduler's comparisons of latency gains are
 # specified in plain IEEE double arithmetic
+# only the C ABI is exported from either library
+EXPORTS = ["-Wl,--version-script=" + os.path.join(CSRC, "exports.map")]
 GXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off", "-Wall", "-Wextra",
-             "-I" + INCLUDE]
+             "-I" + INCLUDE] + EXPORTS
 
 # Packed fp32 VALU instructions are kept out of the generated code on purpose.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-               "-Wall", "-Wno-unused-function", "-I" + INCLUDE, "-I" + CSRC]
+               "-Wall", "-Wno-unused-function", "-I" + INCLUDE, "-I" + CSRC] + EXPORTS
 
 
 def hipcc():

@@ -46,6 +46,9 @@ def test_exports_every_declared_symbol(lib):
                          check=True).stdout
     exported = set(re.findall(r"\bT (ts_\w+)", out))
     assert set(names) <= exported
+    # nothing else: the C++ launch layer and the kernel stubs stay local to the library
+    defined = set(re.findall(r"^[0-9a-fA-F]+ [A-Za-z] (\S+)$", out, flags=re.M))
+    assert defined == set(names), sorted(defined - set(names))
 
 
 def test_abi_version_matches_header(lib):

@@ -252,6 +252,8 @@ def test_exports_every_declared_symbol():
     out = subprocess.run(["nm", "-D", "--defined-only", sched.SCHED_LIB], capture_output=True,
                          text=True, check=True).stdout
     assert set(names) <= set(re.findall(r"\bT (ts_sched_\w+)", out))
+    defined = set(re.findall(r"^[0-9a-fA-F]+ [A-Za-z] (\S+)$", out, flags=re.M))
+    assert defined == set(names), sorted(defined - set(names))  # nothing but the C ABI
     m = re.search(r"#define\s+TS_SCHED_ABI_VERSION\s+(\d+)", open(HEADER).read())
     assert sched.load_sched().ts_sched_abi_version() == int(m.group(1))
 
