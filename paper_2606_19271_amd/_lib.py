@@ -47,6 +47,14 @@ def load():
     return lib
 
 
+def i32(name, x):
+    """x as a C int32 argument; ctypes would silently wrap a larger value, so refuse it."""
+    x = int(x)
+    if not -(1 << 31) <= x < (1 << 31):
+        raise ValueError("%s = %d does not fit the C ABI's int32" % (name, x))
+    return x
+
+
 def status_str(status):
     return load().ts_attn_status_str(int(status)).decode()
 

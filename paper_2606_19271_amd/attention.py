@@ -45,7 +45,8 @@ def ts_attn_fwd(q, k, v, scale=None, out=None):
     lib = _lib.load()
     with torch.cuda.device(q.device):
         stream = torch.cuda.current_stream(q.device).cuda_stream
-        rc = lib.ts_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, L, H, d, s,
+        rc = lib.ts_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _lib.i32("B", B),
+                             _lib.i32("L", L), _lib.i32("H", H), _lib.i32("d", d), s,
                              ctypes.c_void_p(stream))
     _lib.check(rc)
     return out
@@ -75,8 +76,9 @@ def ts_attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale=None, out=None):
     with torch.cuda.device(q.device):
         stream = torch.cuda.current_stream(q.device).cuda_stream
         rc = lib.ts_attn_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
-                                    cu_seqlens.numel() - 1, int(max_seqlen), T, H, d, s,
-                                    ctypes.c_void_p(stream))
+                                    _lib.i32("nseq", cu_seqlens.numel() - 1),
+                                    _lib.i32("max_seqlen", max_seqlen), _lib.i32("T", T),
+                                    _lib.i32("H", H), _lib.i32("d", d), s, ctypes.c_void_p(stream))
     _lib.check(rc)
     return out
 
@@ -128,7 +130,10 @@ def ts_attn_fwd_kvcache(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_s
         rc = lib.ts_attn_fwd_kvcache(_ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                      _ptr(lse) if lse is not None else ctypes.c_void_p(None),
                                      _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
-                                     cu_seqlens_q.numel() - 1, int(max_seqlen_q), int(max_seqlen_k),
-                                     Tq, Tk, H, d, s, int(num_splits), ctypes.c_void_p(stream))
+                                     _lib.i32("nseq", cu_seqlens_q.numel() - 1),
+                                     _lib.i32("max_seqlen_q", max_seqlen_q),
+                                     _lib.i32("max_seqlen_k", max_seqlen_k), _lib.i32("Tq", Tq),
+                                     _lib.i32("Tk", Tk), _lib.i32("H", H), _lib.i32("d", d), s,
+                                     _lib.i32("num_splits", num_splits), ctypes.c_void_p(stream))
     _lib.check(rc)
     return (out, lse) if lse is not None else out

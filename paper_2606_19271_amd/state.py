@@ -45,6 +45,7 @@ def ts_state_copy(src, dst, ranges):
         stream = torch.cuda.current_stream(dev).cuda_stream
         rc = lib.ts_state_copy(ctypes.c_void_p(src.data_ptr()), src.numel() * src.element_size(),
                                ctypes.c_void_p(dst.data_ptr()), dst.numel() * dst.element_size(),
-                               ctypes.c_void_p(r.ctypes.data), r.shape[0], ctypes.c_void_p(stream))
+                               ctypes.c_void_p(r.ctypes.data), _lib.i32("nranges", r.shape[0]),
+                               ctypes.c_void_p(stream))
     _lib.check(rc)
     return dst

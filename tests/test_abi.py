@@ -193,6 +193,15 @@ def test_pack_ranges():
     assert end == 1040 + 560
 
 
+def test_binding_refuses_ints_that_do_not_fit_int32():
+    # ctypes would wrap 2**32 + 64 to 64 without a word; the binding refuses it instead
+    for x in (1 << 31, (1 << 32) + 64, -(1 << 31) - 1):
+        with pytest.raises(ValueError):
+            _lib.i32("L", x)
+    for x in (0, 1, (1 << 31) - 1, -(1 << 31)):
+        assert _lib.i32("L", x) == x
+
+
 def test_python_binding_rejects_cpu_tensors():
     import torch
     x = torch.zeros((1, 8, 1, 64), dtype=torch.bfloat16)

@@ -319,6 +319,16 @@ def test_bad_cu_seqlens_is_a_noop_and_validate_mode_reports_it():
     torch.cuda.synchronize()
 
 
+def test_sizes_beyond_int32_are_refused_by_the_binding():
+    w, q, k, v = draw([64], 1, 64, seed=3)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    cu = torch.tensor(w.cu_seqlens, device="cuda")
+    with pytest.raises(ValueError):
+        ts.ts_attn_fwd_varlen(qd, kd, vd, cu, (1 << 32) + 64)  # would reach the ABI as 64
+    with pytest.raises(ValueError):
+        ts.ts_attn_fwd_kvcache(qd, kd, vd, cu, cu, 64, (1 << 32) + 64)
+
+
 def test_runs_on_a_side_stream():
     seqlens = [400, 123]
     w, q, k, v = draw(seqlens, 2, 128, seed=61)
