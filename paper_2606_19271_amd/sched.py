@@ -78,6 +78,14 @@ def _check(status):
         raise SchedError(status)
 
 
+def _i32(name, x):
+    """x for an int32 field or argument; ctypes would silently wrap a larger value."""
+    x = int(x)
+    if not -(1 << 31) <= x < (1 << 31):
+        raise ValueError("%s = %d does not fit int32" % (name, x))
+    return x
+
+
 class Scheduler:
     """One scheduler instance (ts_sched_create / ts_sched_destroy).
 
@@ -95,11 +103,12 @@ class Scheduler:
             raise ValueError("level table: L rho and lambda values and L - 1 bounds, L <= %d"
                              % MAX_LEVELS)
         prm = _Params()
-        prm.K, prm.m_min, prm.m_max, prm.m_init = K, m_min, m_max, m_init
+        prm.K, prm.m_min = _i32("K", K), _i32("m_min", m_min)
+        prm.m_max, prm.m_init = _i32("m_max", m_max), _i32("m_init", m_init)
         for n, x in enumerate(chunk_latency):
             prm.chunk_latency[n] = float(x)
         prm.eta, prm.mig_alpha_ms, prm.mig_beta_ms_per_byte = float(eta), float(alpha), float(beta)
-        prm.delta, prm.window, prm.levels = float(delta), int(window), L
+        prm.delta, prm.window, prm.levels = float(delta), _i32("window", window), L
         for i in range(L):
             prm.level_lambda[i], prm.level_rho[i] = float(level_lambda[i]), float(level_rho[i])
         for i in range(L - 1):
@@ -125,8 +134,16 @@ class Scheduler:
                 np.ascontiguousarray(a[:, 2]))
 
     def step_packed(self, kinds, ids, nbytes):
-        """One decision epoch from packed arrays; returns the raw ts_sched_decision."""
+        """One decision epoch from packed arrays (contiguous int32 kinds, int64 ids and int64
+        state bytes, one entry per change, as pack() makes them); returns the raw
+        ts_sched_decision, which the next call overwrites."""
         n = len(kinds)
+        for name, a, dt in (("kinds", kinds, np.int32), ("ids", ids, np.int64),
+                            ("nbytes", nbytes, np.int64)):
+            if (not isinstance(a, np.ndarray) or a.dtype != dt or a.ndim != 1 or len(a) != n
+                    or not a.flags["C_CONTIGUOUS"]):
+                raise ValueError("%s must be a contiguous 1-d %s array of %d entries"
+                                 % (name, np.dtype(dt).name, n))
         _check(self._lib.ts_sched_step(self._h, n, kinds.ctypes.data if n else None,
                                        ids.ctypes.data if n else None,
                                        nbytes.ctypes.data if n else None, ctypes.byref(self._dec)))

@@ -245,6 +245,19 @@ def declared(prefix):
     return sorted(set(re.findall(r"\b(%s\w+)\s*\(" % prefix, text)))
 
 
+def test_binding_refuses_wrapped_ints_and_wrong_arrays():
+    lat = [0.0, 10.0, 20.0]
+    with pytest.raises(ValueError):
+        sched.Scheduler(2, 0, (1 << 32) + 4, 1, lat, 1.0)  # ctypes would store m_max = 4
+    s = sched.Scheduler(2, 0, 4, 1, lat, 1.0)
+    kinds, ids, nb = sched.Scheduler.pack([(sched.ARRIVE, 1, 0)])
+    with pytest.raises(ValueError):
+        s.step_packed(kinds.astype(np.int64), ids, nb)  # int64 kinds would be read as int32 pairs
+    with pytest.raises(ValueError):
+        s.step_packed(kinds, ids[:0], nb)
+    assert s.step_packed(kinds, ids, nb).n_req == 1
+
+
 def test_exports_every_declared_symbol():
     names = declared("ts_sched_")
     assert names == ["ts_sched_abi_version", "ts_sched_create", "ts_sched_destroy",
