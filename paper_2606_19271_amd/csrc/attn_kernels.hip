@@ -690,12 +690,13 @@ attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
 template <int D>
 __global__ void __launch_bounds__(kMergeThreads)
 attn_merge_kernel(const float* __restrict__ part_o, const float* __restrict__ part_lse,
-                  int n_split, int64_t rows, __bf16* __restrict__ o, float* __restrict__ lse) {
+                  int n_split, int64_t rows, __bf16* __restrict__ o, float* __restrict__ lse,
+                  const int32_t* __restrict__ plan) {
   constexpr int kChunks = D / 8;
   const int64_t gid = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
   const int64_t row = gid / kChunks;
   const int c8 = (int)(gid % kChunks);
-  if (row >= rows) return;
+  if (row >= rows || plan[1] != 0) return;  // a rejected plan wrote no partials: O stays as is
   float m = -INFINITY;
   for (int i = 0; i < n_split; ++i) m = fmaxf(m, part_lse[i * rows + row]);
   f32x4 a0 = {0.0f, 0.0f, 0.0f, 0.0f}, a1 = a0;
@@ -732,9 +733,13 @@ plan_kernel(const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, 
   int bad = 0;
   if (tid == 0 && (cu_q[0] != 0 || cu_q[nseq] != total_q || cu_k[0] != 0 || cu_k[nseq] != total_k))
     bad = 1;
+  // every offset within [0, total] before any difference is taken: a check of the differences
+  // alone could be passed by offsets that wrap around the int32 range
   for (int s = tid; s < nseq; s += kPlanThreads) {
-    const int lq = cu_q[s + 1] - cu_q[s], lk = cu_k[s + 1] - cu_k[s];
-    if (lq < 0 || lq > max_q || lk < 0 || lk > max_k) bad = 1;
+    const int q0 = cu_q[s], q1 = cu_q[s + 1], k0 = cu_k[s], k1 = cu_k[s + 1];
+    if (q0 < 0 || q1 > total_q || q1 < q0 || q1 - q0 > max_q || k0 < 0 || k1 > total_k ||
+        k1 < k0 || k1 - k0 > max_k)
+      bad = 1;
   }
   if (__syncthreads_or(bad)) {
     if (tid == 0) { plan[0] = 0; plan[1] = 1; }
@@ -835,7 +840,7 @@ static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
   const int64_t threads = rows * (D / 8);
   const int64_t blocks = (threads + kMergeThreads - 1) / kMergeThreads;
   hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
-                     a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse);
+                     a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse, a.plan);
   return hipGetLastError();
 }
 

@@ -195,6 +195,43 @@ def test_kv_workload_sampled(name, n_random):
     assert float(np.abs(got).mean()) > 1e-3  # not an all-zero output
 
 
+def test_kv_rejected_offsets_leave_outputs_untouched():
+    # a rejected plan is a no-op on every path: also with split key ranges, where the merge
+    # kernel must not write O or lse from partials that were never computed
+    w, q, k, v = draw([64, 64], [128, 128], 1, 64, 92)
+    cq = torch.tensor(w.cu_q, device="cuda")
+    bad_k = torch.tensor([0, 200, 256], dtype=torch.int32, device="cuda")  # segment longer than max_k
+    for splits in (1, 3):
+        o = torch.full((w.Tq, 1, 64), 7.0, dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((w.Tq, 1), 123.0, dtype=torch.float32, device="cuda")
+        say("kv rejected offsets, splits", splits)
+        ts.ts_attn_fwd_kvcache(q.cuda(), k.cuda(), v.cuda(), cq, bad_k, w.max_q, 128, out=o, lse=lse,
+                               num_splits=splits)
+        torch.cuda.synchronize()
+        assert bool((o == 7.0).all()) and bool((lse == 123.0).all()), "splits=%d" % splits
+
+
+def test_kv_offsets_that_wrap_int32_are_rejected():
+    # key offsets whose wrapping differences pass a differences-only check (see the packed test)
+    Tk, nseq, max_k = 1024, 512, (1 << 24) - 512
+    diffs = [max_k] * 256 + [(1 << 32) + Tk - 256 * max_k] + [0] * (nseq - 257)
+    ck = [0]
+    for x in diffs:
+        ck.append(((ck[-1] + x + (1 << 31)) % (1 << 32)) - (1 << 31))
+    assert ck[-1] == Tk and min(ck) < 0
+    cq = [0] + [1] * nseq  # one query in the first segment
+    q = torch.randn((1, 1, 64)).to(torch.bfloat16).cuda()
+    kv = torch.randn((Tk, 1, 64)).to(torch.bfloat16).cuda()
+    o = torch.full((1, 1, 64), 7.0, dtype=torch.bfloat16, device="cuda")
+    say("kv wrapping offsets")
+    for splits in (1, 3):
+        ts.ts_attn_fwd_kvcache(q, kv, kv, torch.tensor(cq, dtype=torch.int32, device="cuda"),
+                               torch.tensor(ck, dtype=torch.int32, device="cuda"), 1, max_k, out=o,
+                               num_splits=splits)
+        torch.cuda.synchronize()
+        assert bool((o == 7.0).all()), "splits=%d" % splits
+
+
 def test_kv_bad_offsets_validate_mode():
     w, q, k, v = draw([64, 64], [128, 128], 1, 64, 91)
     cq = torch.tensor(w.cu_q, device="cuda")

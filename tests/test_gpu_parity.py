@@ -319,6 +319,38 @@ def test_bad_cu_seqlens_is_a_noop_and_validate_mode_reports_it():
     torch.cuda.synchronize()
 
 
+def wrapping_offsets(T, nseq, max_len):
+    """Offsets whose int32 differences all lie in [0, max_len] and that start at 0 and end at T,
+    while the offsets in between wrap far outside [0, T] (nseq * max_len >= 2^32)."""
+    diffs = [max_len] * 256 + [(1 << 32) + T - 256 * max_len] + [0] * (nseq - 257)
+    cu = [0]
+    for x in diffs:
+        cu.append(((cu[-1] + x + (1 << 31)) % (1 << 32)) - (1 << 31))
+    assert cu[-1] == T and min(cu) < 0 and max(cu) > T
+    return cu
+
+
+def test_offsets_that_wrap_int32_are_rejected():
+    # regression: the plan once checked only the (wrapping) differences of the offsets, which
+    # these pass; every offset must now lie in [0, T], and the call is a device-side no-op
+    T, H, d, nseq, max_len = 1024, 1, 64, 512, (1 << 24) - 512
+    cu = torch.tensor(wrapping_offsets(T, nseq, max_len), dtype=torch.int32, device="cuda")
+    q = torch.randn((T, H, d)).to(torch.bfloat16).cuda()
+    o = torch.full((T, H, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    say("wrapping offsets", nseq, max_len)
+    ts.ts_attn_fwd_varlen(q, q, q, cu, max_len, out=o)
+    torch.cuda.synchronize()
+    assert bool((o == 7.0).all())
+    os.environ["TS_ATTN_VALIDATE"] = "1"
+    try:
+        with pytest.raises(ts.TsAttnError) as ei:
+            ts.ts_attn_fwd_varlen(q, q, q, cu, max_len, out=o)
+        assert ei.value.status == 10
+    finally:
+        del os.environ["TS_ATTN_VALIDATE"]
+    torch.cuda.synchronize()
+
+
 def test_sizes_beyond_int32_are_refused_by_the_binding():
     w, q, k, v = draw([64], 1, 64, seed=3)
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
