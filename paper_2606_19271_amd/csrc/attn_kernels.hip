@@ -7,8 +7,10 @@
 //
 // Design (one work item = one (segment, head, 256-query tile); one 512-thread workgroup each):
 //  * 8 waves, each owning 32 queries.  The wave computes S^T = K Q^T on 32x32x16 bf16 MFMAs,
-//    so that a lane holds all scores of ONE query (its column): row max and row sum are
-//    in-lane, plus one cross-half exchange (v_permlane32_swap) for the max.
+//    so that a lane holds all scores of ONE query (its column): the row max is in-lane, plus
+//    one cross-half exchange (v_permlane32_swap).  The row sums of the weights are formed on
+//    the matrix core, by a 16x16x32 MFMA per 16 keys with a 0/1 operand that adds the two lanes
+//    of each query.
 //  * The exponentiated scores P^T, packed to bf16, are already the B operand of the next
 //    product O^T += V^T P^T once the keys inside each 16-key step are taken in the order the
 //    accumulator holds them (a sum over keys does not care about their order); V^T's fragments
@@ -18,17 +20,18 @@
 //    issues the softmax VALU work, and they swap roles at each workgroup barrier.  On gfx950
 //    v_exp_f32 shares the VALU pipe with the other vector ops, while MFMAs run in the matrix
 //    core, so the softmax can hide under the other wave's matrix work.
-//  * K and V tiles of 64 keys are staged in LDS in rings of three, laid out (K padded, V
-//    XOR-swizzled) so that the MFMA operand reads are free of bank conflicts.  They arrive by
-//    LDS DMA (buffer_load ... lds), which needs no registers and no LDS write instructions,
-//    issued only in the vector steps; the raw buffer descriptor's range check returns zeros
-//    past the segment's last row.
+//  * K and V tiles of 64 keys are staged in LDS in rings of four (K) and three (V), laid out
+//    (K padded, V XOR-swizzled) so that the MFMA operand reads are free of bank conflicts.  They
+//    arrive by LDS DMA (buffer_load ... lds), which needs no registers and no LDS write
+//    instructions, issued only in the vector steps; the raw buffer descriptor's range check
+//    returns zeros past the segment's last row.  The first K operands of each matrix step are
+//    read at the end of the preceding vector step, so their latency overlaps the barrier.
 //  * Online softmax in the log2 domain (exp2 with scale*log2(e) folded into one FMA).  A tile
 //    is first exponentiated against the running maximum as it stands; only if some weight
-//    would exceed 2^40 (or on the first and the ragged last tile) is the tile's maximum taken
-//    and the O accumulator rescaled.  Keeping a stale maximum is exact in real arithmetic (the
-//    final division by the running sum cancels the common factor), so for ordinary inputs the
-//    per-tile max reduction and the O rescale disappear.
+//    would exceed 2^40 times the largest so far (or on the first and the last tile) is the
+//    tile's maximum taken and the O accumulator rescaled.  Keeping a stale maximum is exact in
+//    real arithmetic (the final division by the running sum cancels the common factor), so for
+//    ordinary inputs the per-tile max reduction and the O rescale disappear.
 //  * Scheduling: the launch has one workgroup per item; blockIdx is remapped so that the 32
 //    workgroups resident at once on one XCD (the hardware deals workgroups to the 8 XCDs
 //    round robin) take 32 consecutive query tiles of the same head and share its K/V in that
@@ -48,6 +51,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
@@ -63,7 +67,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
 
 // LDS layout: a ring of three V tiles (first, so every V address fits the 16-bit immediate of a
-// DS instruction), then a ring of three K tiles; K_j and V_j sit in stage j % 3.  Tiles arrive by
+// DS instruction), then a ring of four K tiles; V_j sits in stage j % 3 and K_j in j % 4.  Tiles arrive by
 // LDS DMA (buffer_load ... lds: lane i of an instruction lands at base + 16 i), 1 KiB per
 // instruction.
 //  * K rows are padded by one 16-byte chunk (stride 2d + 16 bytes), so the 16 rows one b128 K
@@ -78,10 +82,11 @@ struct Geo {
   static constexpr int kVRow = D * 2;                    // V row stride (bytes)
   static constexpr int kKTile = kBN * kKRow;
   static constexpr int kVTile = kBN * kVRow;
-  static constexpr int kStages = 3;
+  static constexpr int kKStages = 4;                     // K_j in stage j % 4
+  static constexpr int kVStages = 3;                     // V_j in stage j % 3
   static constexpr int kVRing = 0;                       // byte offset of the V ring
-  static constexpr int kKRing = kStages * kVTile;        // byte offset of the K ring
-  static constexpr int kLds = kStages * (kKTile + kVTile);
+  static constexpr int kKRing = kVStages * kVTile;       // byte offset of the K ring
+  static constexpr int kLds = kKStages * kKTile + kVStages * kVTile;
   static constexpr int kGroupWaves = kWaves / 2;
   static constexpr int kKDma = kKTile / 1024;            // DMA instructions per K tile (17 / 9)
   static constexpr int kVDma = kVTile / 1024;            // per V tile (16 / 8)
@@ -89,7 +94,7 @@ struct Geo {
   static constexpr int kKDmaMin = kKDma / kGroupWaves;                      // per wave, at least
   static constexpr int kVDmaPerWave = kVDma / kGroupWaves;
   static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && kVDma % kGroupWaves == 0, "DMA split");
-  static_assert(kStages * kVTile <= 65536, "V addresses must fit the DS immediate");
+  static_assert(kVStages * kVTile <= 65536, "V addresses must fit the DS immediate");
   __host__ __device__ static constexpr int vswz(int r) {
     return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
   }
@@ -108,10 +113,6 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 __device__ __forceinline__ float half_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float half_sum(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // One work item: queries [q_begin, q_begin + kBM) of a segment, head h, against the 64-key
@@ -167,20 +168,37 @@ __device__ __forceinline__ int remap_block(int b, int total, int chunk) {
 // Accumulator register r of block kb holds key 32*kb + 8*(r/4) + 4*hb + r%4 of the tile for the
 // lane's query (lane & 31).  The two blocks' MFMAs alternate, so that each Q fragment is the B
 // operand of two consecutive MFMAs: under the power cap an operand held over consecutive MFMAs
-// costs less switching energy, and the clock rises accordingly (measured +0.6 %).
+// costs less switching energy, and the clock rises accordingly (measured +0.6 %).  MFMA i uses
+// the K fragment (kk, kb) = (i / 2, i % 2); the first kPreReads of them were read ahead into kp.
+constexpr int kPreReads = 8;
+
+template <int D>
+__device__ __forceinline__ const lds_char* k_frag(const lds_char* kt, int kk, int kb, int lane) {
+  using G = Geo<D>;
+  return kt + (32 * kb + (lane & 31)) * G::kKRow + (lane >> 5) * 16 + kk * 32;
+}
+
+// The K fragments of a tile's first kPreReads S MFMAs.
+template <int D>
+__device__ __forceinline__ void k_preread(const lds_char* __restrict__ kt, bf16x8 (&kp)[kPreReads],
+                                          int lane) {
+#pragma unroll
+  for (int i = 0; i < kPreReads; ++i)
+    kp[i] = *(const lds_bf16x8*)k_frag<D>(kt, i / 2, i % 2, lane);
+}
+
 template <int D>
 __device__ __forceinline__ void qk_tile(const lds_char* __restrict__ kt, const bf16x8 (&qf)[D / 16],
-                                        f32x16 (&s)[kBN / 32], int lane) {
-  using G = Geo<D>;
-  const int hb = lane >> 5, col = lane & 31;
+                                        const bf16x8 (&kp)[kPreReads], f32x16 (&s)[kBN / 32],
+                                        int lane) {
 #pragma unroll
   for (int kb = 0; kb < kBN / 32; ++kb) s[kb] = f32x16{};
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
     for (int kb = 0; kb < kBN / 32; ++kb) {
-      const lds_char* krow = kt + (32 * kb + col) * G::kKRow + hb * 16;
-      bf16x8 a = *(const lds_bf16x8*)(krow + kk * 32);
+      const int i = 2 * kk + kb;
+      bf16x8 a = i < kPreReads ? kp[i] : *(const lds_bf16x8*)k_frag<D>(kt, kk, kb, lane);
       s[kb] = mfma32(a, qf[kk], s[kb]);
     }
 }
@@ -208,13 +226,37 @@ struct VOffsets {
   }
 };
 
-// O^T += V^T P^T for one 64-key tile.  p[t] holds the bf16 weights of keys
-// 16t + 8*(m/4) + 4*hb + m%4 (m = 0..7) -- the accumulator order of qk_tile -- and the V^T
-// fragments are read in that same key order with the transpose read: elements 0-3 from rows
+// Row sums of the weights on the matrix core: one 16x16x32 MFMA per 16-key step.  The B operand
+// is the step's weight fragment p[t] as it is (lane l: 8 keys of query l & 31), which this MFMA
+// reads as column l & 15, k = 8 (l >> 4) + 0..7; the A operand is 1 on the k-groups {G, G ^ 2}
+// of the rows 4G..4G+3 and 0 elsewhere.  Result row 4G + r, column n is then the sum of lanes
+// 16G + n and 16(G ^ 2) + n -- the two lanes of one query, l and l ^ 32 -- and it lands in
+// exactly those lanes, in all four accumulator registers.  The sum is formed from exactly the
+// bf16 weights the PV product uses, so a row dominated by one key returns that key's value
+// exactly.  Summing in the vector step instead costs two VALU instructions per weight (a pair of
+// bf16 is widened by a shift and a mask and added; v_dot2_f32_bf16 issues to the matrix core and
+// stalls behind the other wave's MFMAs), and that step is the longer of the two.
+
+// A operand of the row-sum MFMA for this lane: bf16 1.0 where the lane's k-group is one of the
+// two groups its row block sums, else 0.
+__device__ __forceinline__ bf16x8 row_sum_selector(int lane) {
+  const int g = lane >> 4, mg = (lane & 15) >> 2;
+  const unsigned one = (g == mg || g == (mg ^ 2)) ? 0x3f803f80u : 0u;
+  return __builtin_bit_cast(bf16x8, u32x4{one, one, one, one});
+}
+
+__device__ __forceinline__ void row_sum_mfma(bf16x8 sel, bf16x8 w, f32x4& l) {
+  l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, w, l, 0, 0, 0);
+}
+
+// O^T += V^T P^T for one 64-key tile, and l += the row sums of P.  p[t] holds the bf16 weights
+// of keys 16t + 8*(m/4) + 4*hb + m%4 (m = 0..7) -- the accumulator order of qk_tile -- and the
+// V^T fragments are read in that same key order with the transpose read: elements 0-3 from rows
 // 16t + 4hb + 0..3, elements 4-7 from rows 16t + 8 + 4hb + 0..3.
 template <int D>
 __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const VOffsets<D>& vo,
-                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32]) {
+                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32],
+                                        bf16x8 sel, f32x4& l) {
   using G = Geo<D>;
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t)
@@ -225,22 +267,20 @@ __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const V
       bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo.off[1][db]));
       bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
       o[db] = mfma32(a, p[t], o[db]);
+      if (db == D / 32 - 1) row_sum_mfma(sel, p[t], l);
     }
 }
 
 // exp2(S*c - m_c) for the 32 scores of the lane, packed to the bf16 B operands of the PV
-// product, with their sum, accumulated in fp32 from the bf16 values the product will use (so a
-// row dominated by one key returns that key's value exactly).  Each packed pair is widened by a
-// shift and a mask and summed with plain fp32 adds: v_dot2_f32_bf16 would do it in one
-// instruction, but it issues to the matrix core and measured up to ~7x slower while the other
-// wave of the SIMD streams MFMAs.
+// product.  Returns the bitwise OR of the packed words: bit 14 of a bf16 is the top bit of its
+// exponent, set exactly when the (non-negative) value is at least 2 or not finite, so
+// (OR & 0x40004000) != 0 flags a tile whose weights are not all below 2.
 template <bool kMasked>
-__device__ __forceinline__ float exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
-                                          float m_c, float c, int keys_valid, int hb) {
-  float lsum[kBN / 16];  // independent partial sums, one per 16-key step
+__device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
+                                             float m_c, float c, int keys_valid, int hb) {
+  unsigned any = 0;
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t) {
-    float pair[4];
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
       float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
@@ -255,39 +295,35 @@ __device__ __forceinline__ float exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&
       bf16x2 pb = __builtin_convertvector(e, bf16x2);
       p[t][m] = pb[0];
       p[t][m + 1] = pb[1];
-      const unsigned u = __builtin_bit_cast(unsigned, pb);
-      pair[m >> 1] = __uint_as_float(u << 16) + __uint_as_float(u & 0xffff0000u);
+      any |= __builtin_bit_cast(unsigned, pb);
     }
-    lsum[t] = (pair[0] + pair[1]) + (pair[2] + pair[3]);
   }
-  float lt = lsum[0];
-#pragma unroll
-  for (int t = 1; t < kBN / 16; ++t) lt += lsum[t];
-  return lt;
+  return any;
 }
 
 // Online softmax of one tile of scores (the lane's query): turns S into bf16 weights
-// P = exp2(S*c - m_c) and adds their sum to l_part.
+// P = exp2(S*c - m_c).  Their sum is accumulated by the matrix step (row_sum_mfma).
 //
-// The running maximum m_c is not recomputed per tile.  A full tile first tries the current
-// m_c: if every lane's weights sum to at most kSumLimit, every weight is at most kSumLimit, the
-// fp32 accumulators stay far from overflow, and the tile is done -- exact in real arithmetic,
-// since the final division by l cancels the common factor 2^(m_true - m_c).  Otherwise (the
-// first tile, where m_c = -inf, a score far above the running maximum, or the masked last tile)
-// the tile's true maximum is taken, m_c moves up to it, `rescale` is set and the O accumulator
-// must be multiplied by `alpha` before these weights are added to it.
-constexpr float kSumLimit = 1099511627776.0f;  // 2^40
+// m_c is the running maximum (log2 units of the scaled scores) raised by kBias, so the largest
+// weight seen so far is 2^-kBias; the bias cancels in O / l and is part of the log-sum-exp.
+// m_c is not recomputed per tile.  A full tile first tries the current m_c: if every weight of
+// every lane is below 2 -- at most 2^(kBias + 1) times the largest weight so far -- the fp32
+// accumulators stay far from overflow and the tile is done; exact in real arithmetic, since the
+// final division by l cancels the common factor.  Otherwise (the first tile, where m_c = -inf, a
+// score far above the running maximum, or the masked last tile) the tile's true maximum is
+// taken, m_c moves up to it (plus the bias), `rescale` is set and the accumulators of O and l
+// must be multiplied by `alpha` before these weights are added to them.
+constexpr float kBias = 39.0f;
 
 template <bool kMasked>
 __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
-                                             float& m_c, float& l_part, float& alpha,
-                                             bool& rescale, float c, int keys_valid, int lane) {
+                                             float& m_c, float& alpha, bool& rescale,
+                                             float c, int keys_valid, int lane) {
   const int hb = lane >> 5;
   if (!kMasked) {
-    const float lt = exp_pack<false>(s, p, m_c, c, kBN, hb);
-    if (__builtin_amdgcn_ballot_w64(!(lt <= kSumLimit)) == 0) {
+    const unsigned any = exp_pack<false>(s, p, m_c, c, kBN, hb);
+    if (__builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) == 0) {
       rescale = false;
-      l_part += lt;
       return;
     }
   }
@@ -306,20 +342,21 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[
 #pragma unroll
     for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[kb][r]);
   mt = half_max(mt);
-  const float m_new = fmaxf(m_c, mt * c);  // c >= 0, so the max commutes with the scaling
+  // c >= 0, so the max commutes with the scaling
+  const float m_new = fmaxf(m_c, __builtin_fmaf(mt, c, kBias));
   alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
   m_c = m_new;
   rescale = true;
-  const float lt = exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
-  l_part = l_part * alpha + lt;
+  exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
 }
 
 template <int D>
-__device__ __forceinline__ void scale_acc(f32x16 (&o)[D / 32], float alpha) {
+__device__ __forceinline__ void scale_acc(f32x16 (&o)[D / 32], f32x4& l, float alpha) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+  l *= alpha;
 }
 
 // Lane offsets (bytes, relative to the tile's first row in global memory) of one wave's share
@@ -392,27 +429,36 @@ __device__ __forceinline__ void block_sync() {
   __asm__ volatile("" ::: "memory");
 }
 
-// The matrix step of tile j: S_j = K_j Q^T followed by O += V_{j-1} P_{j-1}, in one basic
-// block.  The issue order is pinned so that each MFMA's LDS operand was requested about eight
-// MFMAs earlier: 8 K reads up front, then one MFMA followed by the next one or two operand reads.
+// The matrix step of tile j: S_j = K_j Q^T followed by O += V_{j-1} P_{j-1} and the row sums of
+// P_{j-1}, in one basic block.  The K fragments of the first kPreReads MFMAs were read in the
+// vector step before the barrier, so the first MFMA issues at once; after that the issue order
+// is pinned so that each MFMA's LDS operand is requested kPreReads MFMAs earlier (one b128 read
+// per S MFMA, two transpose reads per PV MFMA, none for a row-sum MFMA, which follows the PV
+// MFMAs of its 16-key step).
+template <int D>
+__device__ __forceinline__ constexpr int m_step_reads(int i) {
+  constexpr int kQK = (kBN / 32) * (D / 16);
+  constexpr int kStep = D / 32 + 1;  // PV MFMAs of a 16-key step, then its row sum
+  return i < kQK ? 1 : ((i - kQK) % kStep == D / 32 ? 0 : 2);
+}
+
 template <int D, bool kPV>
 __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
                                        const VOffsets<D>& vo, const bf16x8 (&qf)[D / 16],
-                                       f32x16 (&s)[kBN / 32], const bf16x8 (&p)[kBN / 16],
-                                       f32x16 (&o)[D / 32], int lane) {
-  qk_tile<D>(kt, qf, s, lane);
-  if (kPV) pv_tile<D>(vt, vo, p, o);
-  constexpr int kQK = (kBN / 32) * (D / 16);          // MFMAs of S (16 at d = 128)
-  constexpr int kPVm = kPV ? (kBN / 16) * (D / 32) : 0;  // MFMAs of PV (16 at d = 128)
-  constexpr int kAhead = 8;
-  // reads: kQK single b128 reads, then 2 transpose reads per PV MFMA
-  __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+                                       const bf16x8 (&kp)[kPreReads], f32x16 (&s)[kBN / 32],
+                                       const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32],
+                                       bf16x8 sel, f32x4& l, int lane) {
+  qk_tile<D>(kt, qf, kp, s, lane);
+  if (kPV) pv_tile<D>(vt, vo, p, o, sel, l);
+  constexpr int kQK = (kBN / 32) * (D / 16);                    // MFMAs of S (16 at d = 128)
+  constexpr int kPVm = kPV ? (kBN / 16) * (D / 32 + 1) : 0;  // PV and row-sum MFMAs (20)
 #pragma unroll
   for (int i = 0; i < kQK + kPVm; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    const int next = i + kAhead;  // MFMA whose operand is requested now
-    if (next < kQK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    else if (next < kQK + kPVm) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    const int next = i + kPreReads;  // MFMA whose operands are requested now
+    const int reads = next < kQK + kPVm ? m_step_reads<D>(next) : 0;
+    if (reads == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    else if (reads == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
   }
 }
 
@@ -426,15 +472,18 @@ __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const ld
 // work.  The matrix step raises its wave priority so its MFMAs issue first, and it does no
 // global-memory work at all.
 //
-// K/V staging is by LDS DMA, issued in the vector steps only: group A fetches K_{j+2} in V(j),
-// group B fetches V_{j+2}, and each wave waits for the fetch of its previous vector step right
-// before the barrier that closes V(j).  Phases (A's M(j) = 2j, A's V(j) = B's M(j) = 2j + 1,
-// B's V(j) = 2j + 2): K_m is complete before phase 2m, where A's M(m) first reads it, and
-// V_{m-1} before phase 2m; a stage is refilled only after the barrier that follows its last
-// reader (B's M(m) at 2m + 1 for K_m, B's M(m + 1) at 2m + 3 for V_m), so three stages suffice.
-// Fetches past the segment end read zeros and land in stages nobody reads any more, so the
-// schedule has no branches.  The two groups are separate instantiations, so each has a
-// straight-line schedule.
+// K/V staging is by LDS DMA, issued in the vector steps only: group A fetches K_{j+3} in V(j)
+// into a ring of four stages, group B fetches V_{j+2} into a ring of three, and each wave waits
+// for the fetch of its previous vector step right before the barrier that closes V(j).  Phases
+// (A's M(j) = 2j, A's V(j) = B's M(j) = 2j + 1, B's V(j) = 2j + 2): K_m is complete before
+// phase 2m - 2 and V_{m-1} before phase 2m; a stage is refilled only after the barrier that
+// follows its last reader (B's M(m) at 2m + 1 for K_m, refilled at 2m + 3; B's M(m + 1) at
+// 2m + 3 for V_m, refilled at 2m + 5).  K_{j+1} is therefore complete and visible during
+// phases 2j .. 2j + 2, so both groups read the K fragments of their next matrix step's first
+// MFMAs at the end of V(j), before its barrier; the LDS latency then overlaps the barrier wait
+// instead of delaying the first MFMA.  Fetches past the segment end read zeros and land in
+// stages nobody reads any more, so the schedule has no branches.  The two groups are separate
+// instantiations, so each has a straight-line schedule.
 template <int D, int kMode>
 __device__ __forceinline__ void write_result(const Item& it, const Out& out,
                                              const f32x16 (&oacc)[D / 32], float l_tot, float m_c,
@@ -466,12 +515,14 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   int koff[G::kKDmaMax], voff[G::kVDmaPerWave];
   if (!kGroupB) dma_offsets_k<D>(gw, lane, row_bytes, koff);
   else dma_offsets_v<D>(gw, lane, row_bytes, voff);
-  // this group's fetch of the item's tile j (K for group A, V for group B) into stage j % 3
-  auto fetch = [&](int j, int stage) {
+  // this group's fetch of the item's tile j: K_j (group A) into stage j % 4, V_j (group B) into
+  // stage vstage, which the caller keeps equal to j % 3
+  auto fetch = [&](int j, int vstage) {
     const int key0 = (it.tile_begin + j) * kBN;
-    if (!kGroupB) dma_k<D>(rk, key0, row_bytes, ktile(stage), koff, gw);
-    else dma_v<D>(rv, key0, row_bytes, vtile(stage), voff, gw);
+    if (!kGroupB) dma_k<D>(rk, key0, row_bytes, ktile(j & 3), koff, gw);
+    else dma_v<D>(rv, key0, row_bytes, vtile(vstage), voff, gw);
   };
+  constexpr int kFetchAhead = kGroupB ? 2 : 3;  // tiles between a fetch and its first reader
   constexpr int kFetchWait = kGroupB ? G::kVDmaPerWave : G::kKDmaMin;  // fewest per wave
 
   // Q fragments (B operand of S^T = K Q^T): query col of this wave, channels 16kk + 8hb + 0..7
@@ -489,66 +540,74 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
   f32x16 s[kBN / 32];
   bf16x8 p[kBN / 16];
-  float m_c = -INFINITY, l_part = 0.0f, alpha = 1.0f;
+  bf16x8 kp[kPreReads];  // K fragments of the next matrix step's first MFMAs
+  f32x4 lacc = {};  // row sums of the weights (every element holds the query's sum)
+  const bf16x8 sel = row_sum_selector(lane);
+  float m_c = -INFINITY, alpha = 1.0f;
   bool rescale = false;
 
   const int ntiles = it.ntiles;
   // valid keys of the item's last tile: fewer than kBN only on the segment's ragged last tile
   const int last_keys = min(kBN, it.k_len - (it.tile_begin + ntiles - 1) * kBN);
-  // vector step j: fetch tile j + 2 into stage st2, softmax S_j -> P_j, wait for the fetch of
-  // the previous vector step, barrier; kMasked on the ragged last tile only
-  auto vstep = [&](int j, int st2, auto masked) {
+  // vector step j: fetch tile j + kFetchAhead (a V tile into stage vst2 = (j + 2) % 3), softmax
+  // S_j -> P_j, wait for the fetch of the previous vector step, read the first K fragments of
+  // M(j + 1), barrier; kMasked on the last tile only, which has no M(j + 1) S product
+  auto vstep = [&](int j, int vst2, auto masked) {
     constexpr bool kMasked = decltype(masked)::value;
-    fetch(j + 2, st2);
-    softmax_tile<kMasked>(s, p, m_c, l_part, alpha, rescale, c, kMasked ? last_keys : kBN, lane);
+    fetch(j + kFetchAhead, vst2);
+    softmax_tile<kMasked>(s, p, m_c, alpha, rescale, c, kMasked ? last_keys : kBN, lane);
 #pragma unroll
     for (int i = 0; i < G::kKDmaMax; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
       __builtin_amdgcn_sched_group_barrier(0x002, 6, 3);
     }
     wait_vmem<kFetchWait>();
+    if (!kMasked) k_preread<D>(ktile((j + 1) & 3), kp, lane);
     block_sync();
   };
   using Full = std::false_type;
   using Last = std::true_type;
 
-  // prologue: tiles 0 and 1 of this group's operand, complete before anyone reads them
+  // prologue: tiles 0 .. kFetchAhead - 1 of this group's operand, complete before anyone reads
+  // them
   fetch(0, 0);
   fetch(1, 1);
+  if (!kGroupB) fetch(2, 2);
   wait_vmem<0>();
   block_sync();
+  k_preread<D>(ktile(0), kp, lane);
   if (kGroupB) block_sync();  // group B starts one step behind
 
   // ---- M(0) and V(0)
   __builtin_amdgcn_s_setprio(1);
-  m_step<D, false>(ktile(0), vtile(0), vo, qf, s, p, oacc, lane);
+  m_step<D, false>(ktile(0), vtile(0), vo, qf, kp, s, p, oacc, sel, lacc, lane);
   __builtin_amdgcn_s_setprio(0);
   block_sync();
   if (ntiles == 1)
     vstep(0, 2, Last{});
   else
     vstep(0, 2, Full{});
-  // ---- tiles 1..: stage of tile j is sj = j % 3; V_{j-1} sits in (j + 2) % 3
-  int s0 = 1, s1 = 2, s2 = 0;  // (j, j + 1, j + 2) % 3 for j = 1
+  // ---- tiles 1..: K_j sits in stage j % 4; V_{j-1} in vs = (j + 2) % 3, where V_{j+2} goes next
+  int vs = 0;
   auto tile = [&](int j, auto masked) {
-    if (rescale) scale_acc<D>(oacc, alpha);
+    if (rescale) scale_acc<D>(oacc, lacc, alpha);
     __builtin_amdgcn_s_setprio(1);
-    m_step<D, true>(ktile(s0), vtile(s2), vo, qf, s, p, oacc, lane);
+    m_step<D, true>(ktile(j & 3), vtile(vs), vo, qf, kp, s, p, oacc, sel, lacc, lane);
     __builtin_amdgcn_s_setprio(0);
     block_sync();
-    vstep(j, s2, masked);
-    const int t = s0; s0 = s1; s1 = s2; s2 = t;
+    vstep(j, vs, masked);
+    vs = vs == 2 ? 0 : vs + 1;
   };
   int j = 1;
   for (; j < ntiles - 1; ++j) tile(j, Full{});
   if (j == ntiles - 1) tile(j, Last{});
-  // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = s2 now
-  if (rescale) scale_acc<D>(oacc, alpha);
-  pv_tile<D>(vtile(s2), vo, p, oacc);
+  // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = vs now
+  if (rescale) scale_acc<D>(oacc, lacc, alpha);
+  pv_tile<D>(vtile(vs), vo, p, oacc, sel, lacc);
   if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
   wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
 
-  write_result<D, kMode>(it, out, oacc, half_sum(l_part), m_c, H, qrow, hb);
+  write_result<D, kMode>(it, out, oacc, lacc[0], m_c, H, qrow, hb);
 }
 
 // The epilogue of one wave: O = O / l for its 32 query rows, and the row's natural log-sum-exp
