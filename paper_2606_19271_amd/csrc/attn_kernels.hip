@@ -311,21 +311,20 @@ __device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[kBN / 32], bf16x8
 // accumulators stay far from overflow and the tile is done; exact in real arithmetic, since the
 // final division by l cancels the common factor.  Otherwise (the first tile, where m_c = -inf, a
 // score far above the running maximum, or the masked last tile) the tile's true maximum is
-// taken, m_c moves up to it (plus the bias), `rescale` is set and the accumulators of O and l
-// must be multiplied by `alpha` before these weights are added to them.
+// taken, m_c moves up to it (plus the bias), and the accumulators of O and l -- which hold the
+// products of the earlier tiles, relative to the old m_c -- are multiplied by
+// alpha = 2^(m_c,old - m_c,new) before the next matrix step adds these weights to them.  Doing
+// that here, in the rare slow path of the vector step, keeps the matrix step free of branches.
 constexpr float kBias = 39.0f;
 
-template <bool kMasked>
+template <int D, bool kMasked>
 __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
-                                             float& m_c, float& alpha, bool& rescale,
-                                             float c, int keys_valid, int lane) {
+                                             float& m_c, f32x16 (&o)[D / 32], f32x4& l, float c,
+                                             int keys_valid, int lane) {
   const int hb = lane >> 5;
   if (!kMasked) {
     const unsigned any = exp_pack<false>(s, p, m_c, c, kBN, hb);
-    if (__builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) == 0) {
-      rescale = false;
-      return;
-    }
+    if (__builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) == 0) return;
   }
   if (kMasked) {
 #pragma unroll
@@ -344,19 +343,14 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[
   mt = half_max(mt);
   // c >= 0, so the max commutes with the scaling
   const float m_new = fmaxf(m_c, __builtin_fmaf(mt, c, kBias));
-  alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
+  const float alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 on the first tile (m_c = -inf)
   m_c = m_new;
-  rescale = true;
-  exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
-}
-
-template <int D>
-__device__ __forceinline__ void scale_acc(f32x16 (&o)[D / 32], f32x4& l, float alpha) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
   l *= alpha;
+  exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
 }
 
 // Lane offsets (bytes, relative to the tile's first row in global memory) of one wave's share
@@ -543,19 +537,20 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   bf16x8 kp[kPreReads];  // K fragments of the next matrix step's first MFMAs
   f32x4 lacc = {};  // row sums of the weights (every element holds the query's sum)
   const bf16x8 sel = row_sum_selector(lane);
-  float m_c = -INFINITY, alpha = 1.0f;
-  bool rescale = false;
+  float m_c = -INFINITY;
 
   const int ntiles = it.ntiles;
   // valid keys of the item's last tile: fewer than kBN only on the segment's ragged last tile
   const int last_keys = min(kBN, it.k_len - (it.tile_begin + ntiles - 1) * kBN);
   // vector step j: fetch tile j + kFetchAhead (a V tile into stage vst2 = (j + 2) % 3), softmax
   // S_j -> P_j, wait for the fetch of the previous vector step, read the first K fragments of
-  // M(j + 1), barrier; kMasked on the last tile only, which has no M(j + 1) S product
+  // M(j + 1); kMasked on the last tile only, which has no M(j + 1) S product.  The barrier that
+  // closes the step opens the next iteration, so the loop's branch is taken before it and the
+  // matrix step that follows the barrier starts with its first MFMA.
   auto vstep = [&](int j, int vst2, auto masked) {
     constexpr bool kMasked = decltype(masked)::value;
     fetch(j + kFetchAhead, vst2);
-    softmax_tile<kMasked>(s, p, m_c, alpha, rescale, c, kMasked ? last_keys : kBN, lane);
+    softmax_tile<D, kMasked>(s, p, m_c, oacc, lacc, c, kMasked ? last_keys : kBN, lane);
 #pragma unroll
     for (int i = 0; i < G::kKDmaMax; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
@@ -563,7 +558,6 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
     }
     wait_vmem<kFetchWait>();
     if (!kMasked) k_preread<D>(ktile((j + 1) & 3), kp, lane);
-    block_sync();
   };
   using Full = std::false_type;
   using Last = std::true_type;
@@ -590,7 +584,7 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   // ---- tiles 1..: K_j sits in stage j % 4; V_{j-1} in vs = (j + 2) % 3, where V_{j+2} goes next
   int vs = 0;
   auto tile = [&](int j, auto masked) {
-    if (rescale) scale_acc<D>(oacc, lacc, alpha);
+    block_sync();  // closes V(j - 1)
     __builtin_amdgcn_s_setprio(1);
     m_step<D, true>(ktile(j & 3), vtile(vs), vo, qf, kp, s, p, oacc, sel, lacc, lane);
     __builtin_amdgcn_s_setprio(0);
@@ -602,7 +596,7 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   for (; j < ntiles - 1; ++j) tile(j, Full{});
   if (j == ntiles - 1) tile(j, Last{});
   // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = vs now
-  if (rescale) scale_acc<D>(oacc, lacc, alpha);
+  block_sync();  // closes V(ntiles - 1)
   pv_tile<D>(vtile(vs), vo, p, oacc, sel, lacc);
   if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
   wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
