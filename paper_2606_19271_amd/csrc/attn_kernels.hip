@@ -245,18 +245,22 @@ __device__ __forceinline__ bf16x8 row_sum_selector(int lane) {
   return __builtin_bit_cast(bf16x8, u32x4{one, one, one, one});
 }
 
-__device__ __forceinline__ void row_sum_mfma(bf16x8 sel, bf16x8 w, f32x4& l) {
-  l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, w, l, 0, 0, 0);
+// The row sums of one tile's weights, on two accumulators in turn: switching the matrix core
+// between the 32x32x16 and the 16x16x32 shape costs about 6 clocks each way (measured), so the
+// four row-sum MFMAs are issued together, and two chains keep them from waiting on each other.
+__device__ __forceinline__ void row_sums(bf16x8 sel, const bf16x8 (&p)[kBN / 16], f32x4 (&l)[2]) {
+#pragma unroll
+  for (int t = 0; t < kBN / 16; ++t)
+    l[t & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, p[t], l[t & 1], 0, 0, 0);
 }
 
-// O^T += V^T P^T for one 64-key tile, and l += the row sums of P.  p[t] holds the bf16 weights
+// O^T += V^T P^T for one 64-key tile.  p[t] holds the bf16 weights
 // of keys 16t + 8*(m/4) + 4*hb + m%4 (m = 0..7) -- the accumulator order of qk_tile -- and the
 // V^T fragments are read in that same key order with the transpose read: elements 0-3 from rows
 // 16t + 4hb + 0..3, elements 4-7 from rows 16t + 8 + 4hb + 0..3.
 template <int D>
 __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const VOffsets<D>& vo,
-                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32],
-                                        bf16x8 sel, f32x4& l) {
+                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32]) {
   using G = Geo<D>;
 #pragma unroll
   for (int t = 0; t < kBN / 16; ++t)
@@ -267,7 +271,6 @@ __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const V
       bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo.off[1][db]));
       bf16x8 a = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
       o[db] = mfma32(a, p[t], o[db]);
-      if (db == D / 32 - 1) row_sum_mfma(sel, p[t], l);
     }
 }
 
@@ -302,7 +305,7 @@ __device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[kBN / 32], bf16x8
 }
 
 // Online softmax of one tile of scores (the lane's query): turns S into bf16 weights
-// P = exp2(S*c - m_c).  Their sum is accumulated by the matrix step (row_sum_mfma).
+// P = exp2(S*c - m_c).  Their sum is accumulated by the matrix step (row_sums).
 //
 // m_c is the running maximum (log2 units of the scaled scores) raised by kBias, so the largest
 // weight seen so far is 2^-kBias; the bias cancels in O / l and is part of the log-sum-exp.
@@ -319,7 +322,7 @@ constexpr float kBias = 39.0f;
 
 template <int D, bool kMasked>
 __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
-                                             float& m_c, f32x16 (&o)[D / 32], f32x4& l, float c,
+                                             float& m_c, f32x16 (&o)[D / 32], f32x4 (&l)[2], float c,
                                              int keys_valid, int lane) {
   const int hb = lane >> 5;
   if (!kMasked) {
@@ -349,7 +352,8 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-  l *= alpha;
+  l[0] *= alpha;
+  l[1] *= alpha;
   exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
 }
 
@@ -423,17 +427,18 @@ __device__ __forceinline__ void block_sync() {
   __asm__ volatile("" ::: "memory");
 }
 
-// The matrix step of tile j: S_j = K_j Q^T followed by O += V_{j-1} P_{j-1} and the row sums of
-// P_{j-1}, in one basic block.  The K fragments of the first kPreReads MFMAs were read in the
-// vector step before the barrier, so the first MFMA issues at once; after that the issue order
-// is pinned so that each MFMA's LDS operand is requested kPreReads MFMAs earlier (one b128 read
-// per S MFMA, two transpose reads per PV MFMA, none for a row-sum MFMA, which follows the PV
-// MFMAs of its 16-key step).
-template <int D>
+// The matrix step of tile j: the row sums of P_{j-1}, S_j = K_j Q^T, then O += V_{j-1} P_{j-1},
+// in one basic block.  None of the first MFMAs waits for the LDS: the row sums read registers
+// only, and the K fragments of the first kPreReads S MFMAs were read in the vector step before
+// the barrier.  After that the issue order is pinned so that each MFMA's LDS operand is
+// requested kPreReads MFMAs earlier (one b128 read per S MFMA, two transpose reads per PV MFMA).
+template <int D, bool kPV>
 __device__ __forceinline__ constexpr int m_step_reads(int i) {
+  constexpr int kRS = kPV ? kBN / 16 : 0;  // row-sum MFMAs
   constexpr int kQK = (kBN / 32) * (D / 16);
-  constexpr int kStep = D / 32 + 1;  // PV MFMAs of a 16-key step, then its row sum
-  return i < kQK ? 1 : ((i - kQK) % kStep == D / 32 ? 0 : 2);
+  if (i < kRS) return 0;
+  i -= kRS;
+  return i < kQK ? (i < kPreReads ? 0 : 1) : 2;
 }
 
 template <int D, bool kPV>
@@ -441,16 +446,17 @@ __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const ld
                                        const VOffsets<D>& vo, const bf16x8 (&qf)[D / 16],
                                        const bf16x8 (&kp)[kPreReads], f32x16 (&s)[kBN / 32],
                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32],
-                                       bf16x8 sel, f32x4& l, int lane) {
+                                       bf16x8 sel, f32x4 (&l)[2], int lane) {
+  if (kPV) row_sums(sel, p, l);
   qk_tile<D>(kt, qf, kp, s, lane);
-  if (kPV) pv_tile<D>(vt, vo, p, o, sel, l);
-  constexpr int kQK = (kBN / 32) * (D / 16);                    // MFMAs of S (16 at d = 128)
-  constexpr int kPVm = kPV ? (kBN / 16) * (D / 32 + 1) : 0;  // PV and row-sum MFMAs (20)
+  if (kPV) pv_tile<D>(vt, vo, p, o);
+  // MFMAs: row sums (4), S (16 at d = 128), PV (16 at d = 128)
+  constexpr int kN = (kPV ? kBN / 16 : 0) + (kBN / 32) * (D / 16) + (kPV ? (kBN / 16) * (D / 32) : 0);
 #pragma unroll
-  for (int i = 0; i < kQK + kPVm; ++i) {
+  for (int i = 0; i < kN; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     const int next = i + kPreReads;  // MFMA whose operands are requested now
-    const int reads = next < kQK + kPVm ? m_step_reads<D>(next) : 0;
+    const int reads = next < kN ? m_step_reads<D, kPV>(next) : 0;
     if (reads == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     else if (reads == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
   }
@@ -535,7 +541,7 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   f32x16 s[kBN / 32];
   bf16x8 p[kBN / 16];
   bf16x8 kp[kPreReads];  // K fragments of the next matrix step's first MFMAs
-  f32x4 lacc = {};  // row sums of the weights (every element holds the query's sum)
+  f32x4 lacc[2] = {};  // row sums of the weights, two chains (every element: the query's sum)
   const bf16x8 sel = row_sum_selector(lane);
   float m_c = -INFINITY;
 
@@ -597,11 +603,12 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   if (j == ntiles - 1) tile(j, Last{});
   // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = vs now
   block_sync();  // closes V(ntiles - 1)
-  pv_tile<D>(vtile(vs), vo, p, oacc, sel, lacc);
+  row_sums(sel, p, lacc);
+  pv_tile<D>(vtile(vs), vo, p, oacc);
   if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
   wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
 
-  write_result<D, kMode>(it, out, oacc, lacc[0], m_c, H, qrow, hb);
+  write_result<D, kMode>(it, out, oacc, lacc[0][0] + lacc[1][0], m_c, H, qrow, hb);
 }
 
 // The epilogue of one wave: O = O / l for its 32 query rows, and the row's natural log-sum-exp
