@@ -173,8 +173,9 @@ def test_peaked_scores_full():
 
 
 def test_increasing_scores_force_rescale():
-    # K rows grow along the sequence so every tile raises the row max well past the lazy
-    # threshold: the rescale branch runs on every tile
+    # K rows grow along the sequence, so every tile raises the row max (by about 6 log2 units)
+    # and every seventh or so passes the 2^40 headroom of the lazy maximum: the slow path then
+    # rescales O and l in the middle of the sequence, several times
     L, H, d = 1024, 1, 128
     g = torch.Generator().manual_seed(3)
     q = torch.ones((L, H, d)).to(torch.bfloat16)
