@@ -189,6 +189,33 @@ def test_increasing_scores_force_rescale():
     assert_parity(as_f64(o), ref, "forced rescale")
 
 
+
+@pytest.mark.parametrize("gap", [5.0, 38.0, 45.0, 200.0, 1000.0])
+def test_score_jump_mid_sequence(gap):
+    # One key in the middle of a segment (key 400, tile 6) scores `gap` log2 units above every
+    # other key of every query row.  Below 40 the lazy maximum stays and the weights are up to
+    # 2^gap times the earlier ones; above it the slow path must take the tile's maximum and
+    # rescale O and l (without it, gap >= 167 overflows the fp32 weights).
+    seqlens = [640, 300]
+    H, d = 2, 128
+    g = torch.Generator().manual_seed(57)
+    T = sum(seqlens)
+    q = torch.randn((T, H, d), generator=g)
+    q[:, :, 0] = 4.0
+    k = 0.3 * torch.randn((T, H, d), generator=g)
+    k[:, :, 0] = 0.0
+    v = torch.randn((T, H, d), generator=g)
+    scale = W.Workload("x", tuple(seqlens), H, d, 0).scale
+    c = float(np.float32(scale)) * 1.4426950408889634
+    k[400, :, 0] = gap / (4.0 * c)
+    q, k, v = q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+    say("score jump", gap)
+    ref = oracle_full(q, k, v, seqlens, scale)
+    o = run_varlen(q, k, v, seqlens)
+    got = as_f64(o)
+    assert np.all(np.isfinite(got))
+    assert_parity(got, ref, "score jump %g" % gap)
+
 # ------------------------------------------------------------------------- full-size workloads
 
 @pytest.mark.parametrize("name", ["dit_small", "dit_large", "highres", "varlen_serving"])
