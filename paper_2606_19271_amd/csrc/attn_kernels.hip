@@ -489,7 +489,13 @@ __device__ __forceinline__ void write_result(const Item& it, const Out& out,
                                              const f32x16 (&oacc)[D / 32], float l_tot, float m_c,
                                              int H, int qrow, int hb);
 
-template <int D, bool kGroupB, int kMode>
+//
+// kActive = false is the same schedule for a wave whose 32 queries all lie past the segment's end
+// (in a ragged last query tile): it issues its share of the K/V DMA, waits for it and takes every
+// barrier, so the workgroup's schedule is unchanged, but it skips the MFMA, softmax and LDS-read
+// work and writes nothing.  Under the power cap the idle matrix and vector work is worth clock
+// to the rest of the chip.
+template <int D, bool kGroupB, int kMode, bool kActive>
 __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __restrict__ q,
                                                const __bf16* __restrict__ k,
                                                const __bf16* __restrict__ v, const Out& out,
@@ -530,7 +536,9 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   bf16x8 qf[D / 16];
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
-    u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(rq, qrow * row_bytes + (2 * kk + hb) * 16, 0, 0);
+    u32x4 raw = {};
+    if constexpr (kActive)
+      raw = __builtin_amdgcn_raw_buffer_load_b128(rq, qrow * row_bytes + (2 * kk + hb) * 16, 0, 0);
     if (negate_q) raw ^= u32x4{0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u};
     qf[kk] = __builtin_bit_cast(bf16x8, raw);
   }
@@ -556,14 +564,15 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   auto vstep = [&](int j, int vst2, auto masked) {
     constexpr bool kMasked = decltype(masked)::value;
     fetch(j + kFetchAhead, vst2);
-    softmax_tile<D, kMasked>(s, p, m_c, oacc, lacc, c, kMasked ? last_keys : kBN, lane);
+    if constexpr (kActive)
+      softmax_tile<D, kMasked>(s, p, m_c, oacc, lacc, c, kMasked ? last_keys : kBN, lane);
 #pragma unroll
     for (int i = 0; i < G::kKDmaMax; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
       __builtin_amdgcn_sched_group_barrier(0x002, 6, 3);
     }
     wait_vmem<kFetchWait>();
-    if (!kMasked) k_preread<D>(ktile((j + 1) & 3), kp, lane);
+    if (kActive && !kMasked) k_preread<D>(ktile((j + 1) & 3), kp, lane);
   };
   using Full = std::false_type;
   using Last = std::true_type;
@@ -575,13 +584,15 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   if (!kGroupB) fetch(2, 2);
   wait_vmem<0>();
   block_sync();
-  k_preread<D>(ktile(0), kp, lane);
+  if constexpr (kActive) k_preread<D>(ktile(0), kp, lane);
   if (kGroupB) block_sync();  // group B starts one step behind
 
   // ---- M(0) and V(0)
-  __builtin_amdgcn_s_setprio(1);
-  m_step<D, false>(ktile(0), vtile(0), vo, qf, kp, s, p, oacc, sel, lacc, lane);
-  __builtin_amdgcn_s_setprio(0);
+  if constexpr (kActive) {
+    __builtin_amdgcn_s_setprio(1);
+    m_step<D, false>(ktile(0), vtile(0), vo, qf, kp, s, p, oacc, sel, lacc, lane);
+    __builtin_amdgcn_s_setprio(0);
+  }
   block_sync();
   if (ntiles == 1)
     vstep(0, 2, Last{});
@@ -591,9 +602,11 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   int vs = 0;
   auto tile = [&](int j, auto masked) {
     block_sync();  // closes V(j - 1)
-    __builtin_amdgcn_s_setprio(1);
-    m_step<D, true>(ktile(j & 3), vtile(vs), vo, qf, kp, s, p, oacc, sel, lacc, lane);
-    __builtin_amdgcn_s_setprio(0);
+    if constexpr (kActive) {
+      __builtin_amdgcn_s_setprio(1);
+      m_step<D, true>(ktile(j & 3), vtile(vs), vo, qf, kp, s, p, oacc, sel, lacc, lane);
+      __builtin_amdgcn_s_setprio(0);
+    }
     block_sync();
     vstep(j, vs, masked);
     vs = vs == 2 ? 0 : vs + 1;
@@ -603,12 +616,15 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   if (j == ntiles - 1) tile(j, Last{});
   // ---- M(ntiles): the last product, V_{ntiles-1} in stage (ntiles - 1) % 3 = vs now
   block_sync();  // closes V(ntiles - 1)
-  row_sums(sel, p, lacc);
-  pv_tile<D>(vtile(vs), vo, p, oacc);
+  if constexpr (kActive) {
+    row_sums(sel, p, lacc);
+    pv_tile<D>(vtile(vs), vo, p, oacc);
+  }
   if (!kGroupB) block_sync();  // matches group B's extra barrier at the start
   wait_vmem<0>();  // the fetches past the end must land before the workgroup leaves
 
-  write_result<D, kMode>(it, out, oacc, lacc[0][0] + lacc[1][0], m_c, H, qrow, hb);
+  if constexpr (kActive)
+    write_result<D, kMode>(it, out, oacc, lacc[0][0] + lacc[1][0], m_c, H, qrow, hb);
 }
 
 // The epilogue of one wave: O = O / l for its 32 query rows, and the row's natural log-sum-exp
@@ -676,10 +692,14 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
                            lane >> 5);
     return;
   }
-  if (wave >= kWaves / 2)
-    run_item_group<D, true, kMode>(it, q, k, v, out, H, c, negate_q, smem);
-  else
-    run_item_group<D, false, kMode>(it, q, k, v, out, H, c, negate_q, smem);
+  const bool active = it.q_begin + 32 * wave < it.q_len;  // some query of this wave is in range
+  if (wave >= kWaves / 2) {
+    if (active) run_item_group<D, true, kMode, true>(it, q, k, v, out, H, c, negate_q, smem);
+    else run_item_group<D, true, kMode, false>(it, q, k, v, out, H, c, negate_q, smem);
+  } else {
+    if (active) run_item_group<D, false, kMode, true>(it, q, k, v, out, H, c, negate_q, smem);
+    else run_item_group<D, false, kMode, false>(it, q, k, v, out, H, c, negate_q, smem);
+  }
 }
 
 template <int D>
