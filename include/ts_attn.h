@@ -31,7 +31,9 @@
  *  - Ownership: the caller owns every buffer; the library keeps no pointer after returning.
  *  - Errors: argument checks run on the host before any HIP call and return a ts_status
  *    without touching the device.  Empty problems (B, L, T or nseq equal to 0) are no-ops
- *    returning TS_OK.  A device that is not gfx950 gives TS_ERR_UNSUPPORTED.
+ *    returning TS_OK.  A tensor of zero rows is never dereferenced, so its pointer may be
+ *    NULL: q, k, v, o when B*L or T is 0; in the chunk call q and o when total_q is 0 and k
+ *    and v when total_k is 0.  A device that is not gfx950 gives TS_ERR_UNSUPPORTED.
  *  - Determinism: results are bitwise reproducible for fixed inputs on one device (no atomics
  *    in the arithmetic, fixed reduction order), and a row's result does not depend on the
  *    other segments of the batch.

@@ -99,9 +99,11 @@ bool ranges_overlap(const void* a, int64_t na, const void* b, int64_t nb) {
 }
 
 // Shared checks of both entry points; tokens = rows of q/k/v/o, longest = longest segment.
+// Tensors of zero rows are never dereferenced, so their pointers may be NULL (torch gives an
+// empty tensor a NULL data pointer).
 int check_common(const void* q, const void* k, const void* v, const void* o, int64_t tokens,
                  int64_t longest, int32_t H, int32_t d, float scale) {
-  if (!q || !k || !v || !o) return TS_ERR_NULL;
+  if (tokens > 0 && (!q || !k || !v || !o)) return TS_ERR_NULL;
   if (H < 1 || tokens < 0 || longest < 0) return TS_ERR_SHAPE;
   if (d != 64 && d != 128) return TS_ERR_HEAD_DIM;
   if (!isfinite(scale)) return TS_ERR_SCALE;
@@ -122,11 +124,12 @@ bool validate_mode() {
 }
 
 // Checks of the chunk-vs-cache call: q/o hold tq rows, k/v tk rows; segments are at most
-// max_q queries and max_k keys long.
+// max_q queries and max_k keys long.  As in check_common, q/o may be NULL when tq = 0 and k/v
+// when tk = 0 (queries without keys read no key: O = 0, lse = -inf).
 int check_kv(const void* q, const void* k, const void* v, const void* o, const float* lse,
              int64_t tq, int64_t tk, int64_t max_q, int64_t max_k, int32_t H, int32_t d,
              float scale) {
-  if (!q || !k || !v || !o) return TS_ERR_NULL;
+  if ((tq > 0 && (!q || !o)) || (tk > 0 && (!k || !v))) return TS_ERR_NULL;
   if (H < 1 || tq < 0 || tk < 0 || max_q < 0 || max_k < 0) return TS_ERR_SHAPE;
   if (d != 64 && d != 128) return TS_ERR_HEAD_DIM;
   if (!isfinite(scale)) return TS_ERR_SCALE;

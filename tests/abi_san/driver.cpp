@@ -83,6 +83,13 @@ int main() {
               expect(s == TS_ERR_SHAPE, "varlen huge H", nseq, maxl, total);
           }
   expect(ts_attn_fwd_varlen(q, k, v, o, nullptr, 1, 64, 64, 2, 64, 1.0f, nullptr) == TS_ERR_NULL, "null cu", 0, 0, 0);
+  // tensors of zero rows may be NULL (an empty torch tensor has a NULL data pointer)
+  expect(ts_attn_fwd(nullptr, nullptr, nullptr, nullptr, 0, 64, 2, 64, 1.0f, nullptr) == TS_OK, "empty dense, NULL tensors", 0, 0, 0);
+  expect(ts_attn_fwd_varlen(nullptr, nullptr, nullptr, nullptr, cu, 2, 0, 0, 2, 64, 1.0f, nullptr) == TS_OK, "empty packed, NULL tensors", 0, 0, 0);
+  expect(ts_attn_fwd_varlen(nullptr, k, v, o, cu, 1, 64, 64, 2, 64, 1.0f, nullptr) == TS_ERR_NULL, "NULL q with rows", 0, 0, 0);
+  expect(ts_attn_fwd_kvcache(nullptr, nullptr, nullptr, nullptr, nullptr, cu, cu, 1, 0, 0, 0, 0, 2, 64, 1.0f, 0, nullptr) == TS_OK, "empty chunk, NULL tensors", 0, 0, 0);
+  expect(ts_attn_fwd_kvcache(q, nullptr, nullptr, o, nullptr, cu, cu, 1, 64, 0, 64, 0, 2, 80, 1.0f, 0, nullptr) == TS_ERR_HEAD_DIM, "NULL k/v of zero rows", 0, 0, 0);
+  expect(ts_attn_fwd_kvcache(q, nullptr, v, o, nullptr, cu, cu, 1, 64, 64, 64, 64, 2, 64, 1.0f, 0, nullptr) == TS_ERR_NULL, "NULL k with rows", 0, 0, 0);
 
   // chunk vs cache: ts_attn_fwd_kvcache(nseq, max_q, max_k, total_q, total_k, H, d, splits)
   const std::vector<int32_t> few = {I32MIN, -1, 0, 1, 257, 65279, 1 << 27, I32MAX};

@@ -118,13 +118,20 @@ def test_dense_argument_checks(lib):
         assert fwd(lib, H=H, L=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
         assert varlen(lib, H=H, max_seqlen=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
         assert kvcache(lib, H=H, max_k=(1 << 31) - 1) == _lib.TS_ERR_SHAPE
-    # empty problems are no-ops that never touch the device
+    # empty problems are no-ops that never touch the device, also with NULL tensors (an empty
+    # torch tensor has a NULL data pointer)
     assert fwd(lib, B=0) == _lib.TS_OK
     assert fwd(lib, L=0) == _lib.TS_OK
+    assert fwd(lib, q=0, k=0, v=0, o=0, B=0) == _lib.TS_OK
+    assert fwd(lib, q=0, k=0, v=0, o=0, L=0) == _lib.TS_OK
+    assert fwd(lib, k=0, B=3, L=0) == _lib.TS_OK
 
 
 def test_varlen_argument_checks(lib):
     assert varlen(lib, cu=0) == _lib.TS_ERR_NULL
+    assert varlen(lib, q=0) == _lib.TS_ERR_NULL
+    assert varlen(lib, q=0, k=0, v=0, o=0, T=0) == _lib.TS_OK   # empty batch, empty tensors
+    assert varlen(lib, q=0, k=0, v=0, o=0, T=0, d=80) == _lib.TS_ERR_HEAD_DIM
     assert varlen(lib, nseq=-1) == _lib.TS_ERR_SHAPE
     assert varlen(lib, max_seqlen=-1) == _lib.TS_ERR_SHAPE
     assert varlen(lib, T=-1) == _lib.TS_ERR_SHAPE
@@ -165,6 +172,16 @@ def test_kvcache_argument_checks(lib):
     # empty problems are no-ops that never touch the device
     assert kvcache(lib, nseq=0) == _lib.TS_OK
     assert kvcache(lib, tq=0) == _lib.TS_OK
+    assert kvcache(lib, q=0, o=0, tq=0) == _lib.TS_OK
+    assert kvcache(lib, q=0, k=0, v=0, o=0, tq=0, tk=0) == _lib.TS_OK
+    # NULL k/v of zero rows pass the pointer check (a later host check, d = 80, shows it without
+    # reaching the device); NULL tensors with rows do not
+    assert kvcache(lib, k=0, v=0, tk=0, max_k=0, d=80) == _lib.TS_ERR_HEAD_DIM
+    assert kvcache(lib, k=0, tk=0, max_k=0, d=80) == _lib.TS_ERR_HEAD_DIM
+    assert kvcache(lib, k=0, v=0, d=80) == _lib.TS_ERR_NULL
+    assert kvcache(lib, q=0, tq=128) == _lib.TS_ERR_NULL
+    assert kvcache(lib, o=0) == _lib.TS_ERR_NULL
+    assert kvcache(lib, k=0, tq=0) == _lib.TS_ERR_NULL   # k has rows: its pointer is required
 
 
 def state_copy(lib, src=A, sb=1 << 20, dst=BIG, db=1 << 20, ranges=((0, 0, 256),), n=None):

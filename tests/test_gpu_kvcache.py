@@ -243,3 +243,36 @@ def test_kv_bad_offsets_validate_mode():
         assert ei.value.status == 10
     finally:
         del os.environ["TS_ATTN_VALIDATE"]
+
+
+@pytest.mark.parametrize("splits", [0, 1, 3])
+def test_kv_no_keys_at_all(splits):
+    # queries but no keys anywhere: k and v are empty tensors (NULL data pointers), and every
+    # row is the empty sum: O = 0, lse = -inf
+    H, d, Tq = 2, 128, 300
+    g = torch.Generator().manual_seed(8)
+    q = torch.randn((Tq, H, d), generator=g).to(torch.bfloat16).cuda()
+    k = torch.empty((0, H, d), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty((0, H, d), dtype=torch.bfloat16, device="cuda")
+    cq = torch.tensor([0, 100, 300], dtype=torch.int32, device="cuda")
+    ck = torch.tensor([0, 0, 0], dtype=torch.int32, device="cuda")
+    say("no keys", splits)
+    o, lse = ts.ts_attn_fwd_kvcache(q, k, v, cq, ck, 200, 0, return_lse=True, num_splits=splits)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(o.float()).item() == 0
+    assert bool(torch.all(torch.isneginf(lse)).item())
+
+
+def test_empty_batches_are_no_ops():
+    # a coalesced batch without tokens: empty tensors (NULL data pointers) are accepted
+    H, d = 2, 128
+    e = torch.empty((0, H, d), dtype=torch.bfloat16, device="cuda")
+    cu = torch.tensor([0, 0, 0], dtype=torch.int32, device="cuda")
+    say("empty batches")
+    o = ts.ts_attn_fwd_varlen(e, e, e, cu, 0)
+    assert o.shape == (0, H, d)
+    o = ts.ts_attn_fwd(e.view(0, 1, H, d), e.view(0, 1, H, d), e.view(0, 1, H, d))
+    assert o.numel() == 0
+    o, lse = ts.ts_attn_fwd_kvcache(e, e, e, cu, cu, 0, 0, return_lse=True)
+    assert o.shape == (0, H, d) and lse.shape == (0, H)
+    torch.cuda.synchronize()
