@@ -402,6 +402,9 @@ def main():
                    "kernel_ms_mean": kernel_ms, "kernel_ms_min": float(np.min(launch_ms)),
                    "kernel_ms_max": float(np.max(launch_ms)),
                    "pct_bf16_peak": 100.0 * achieved / PEAK_BF16_TFLOPS,
+                   # HBM bytes per launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE passes of this
+                   # kernel source (null when they were taken on another source), over the launch
+                   "hbm_GBps_rocprof": None if traffic is None else traffic / (kernel_ms * 1e-3) / 1e9,
                    **({"gemm_bf16_reference": gemm,
                        "value_over_gemm": value / gemm["tflops"]} if gemm else {})},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
