@@ -270,6 +270,55 @@ def pin_closed_loop_trace(mod):
     assert groups(s) == {1: [3, 4], 3: [2, 5], 4: [1]}
 
 
+def pin_scale_direction_bounds_target(mod):
+    """Sec. 5.2.2: the hysteresis band decides the direction of a scaling step and the
+    proportional rule M_tar = ceil(N_req / (K rho*)) its size.  A scale-out that would lower M,
+    or a scale-in that would raise it, contradicts the direction the band chose, so the target is
+    bounded by M(t-) on the side the band points away from.
+
+    Reachable scale-out case by hand: K = 4, l = (0, 150, 200, 260, 330), rho* = 0.5, delta = 0.1
+    (band [0.4, 0.6]), budget 1..3 starting at 3, kappa = 10^6 ms per session (no move can pay).
+    E1: sessions 1..12 arrive round robin, (4,4,4), rho 1.0 > 0.6: M_tar = ceil(12/2) = 6,
+    clamped to m_max = 3: no change.  E2: every session of g1 and g2 departs, (4,0,0): moving one
+    gains 330 - max(l(3), l(1)) - 10^6 < 0, nothing moves; rho 1.0 > 0.6 is a scale-out, while
+    ceil(4/2) = 2 < 3: M stays 3 and nothing is removed.
+
+    Scale-in: with every active session placed, N_req <= M n_max, so rho_max < rho* - delta gives
+    N_req / (K rho*) < M and ceil(...) <= M: the bound never binds on a reachable state.  It is
+    pinned on the controller itself: rho_max = 0.1 (below the band) with a proportional target of
+    ceil(100/2) = 50 GPUs for M = 2 is a scale-in, which removes no GPU and so adds none either."""
+    s = make(mod, m_min=1, m_max=3, m_init=3, alpha=1e6)
+    d = s.step(arrive(*range(1, 13)))
+    assert groups(s) == {0: [1, 4, 7, 10], 1: [2, 5, 8, 11], 2: [3, 6, 9, 12]}
+    assert (d["m"], d["m_target"]) == (3, 3)
+    d = s.step(ev(SR.DEPART, 2, 5, 8, 11, 3, 6, 9, 12))
+    assert (d["rho_max"], d["n_req"], d["migrations"]) == (1.0, 4, 0)
+    assert (d["m"], d["m_target"]) == (3, 3)
+    assert groups(s) == {0: [1, 4, 7, 10], 1: [], 2: []}
+    s = make(mod, m_min=1, m_max=100, m_init=2)
+    assert s.target(100) == 50
+    assert s.scale(0.1, 2, 100) == 2          # scale-in: min(50, 2)
+    assert s.scale(0.9, 60, 100) == 60        # scale-out: max(50, 60)
+    assert s.scale(0.9, 2, 100) == 50 and s.scale(0.1, 60, 100) == 50
+    assert s.scale(0.5, 2, 100) == 2          # inside the band: M unchanged
+
+
+def pin_gmax_lowest_id_tie(mod):
+    """Sec. 5.2.1 leaves g_max in argmax_j l(n_j); the reading takes the lowest-id GPU at the
+    bottleneck.  By hand: K = 4, l = (0, 150, 200, 260, 330), budget fixed at three GPUs, free
+    migration.  E1: sessions 1..9 round robin, (3,3,3).  E2: sessions 3 and 9 of g2 depart,
+    (3,3,1): g0 and g1 share the bottleneck 260; g_max = g0, and moving its lowest session (1)
+    to g2 gives L' = max(l(2), l(2)) = 200 < 260 (the move to g1 would give l(4)).  Then (2,3,2):
+    g_max = g1, and its best move gives L' = max(l(2), l(3)) = 260, no gain: stop, with session 1
+    on g2 (taking g1 first would have moved session 2 instead)."""
+    s = make(mod, m_min=3, m_max=3, m_init=3)
+    s.step(arrive(*range(1, 10)))
+    assert groups(s) == {0: [1, 4, 7], 1: [2, 5, 8], 2: [3, 6, 9]}
+    d = s.step(ev(SR.DEPART, 3, 9))
+    assert d["migrations"] == 1 and d["bottleneck_ms"] == 260.0
+    assert groups(s) == {0: [4, 7], 1: [2, 5, 8], 2: [1, 6]}
+
+
 def pin_pending_when_full(mod):
     """K = 2, budget fixed at one GPU: the third active session has to wait."""
     s = make(mod, K=2, lat=[0.0, 100.0, 150.0], m_min=1, m_max=1)
@@ -346,8 +395,8 @@ def pin_invariants(mod):
 
 PINS = [pin_app_a_table, pin_volatility_numpy, pin_activations_count, pin_target_budget,
         pin_placement_optimal, pin_assignment_and_gain, pin_assignment_prefers_less_loaded,
-        pin_hysteresis_band, pin_migration_cost_blocks,
-        pin_closed_loop_trace, pin_pending_when_full, pin_parameter_delay,
+        pin_hysteresis_band, pin_migration_cost_blocks, pin_scale_direction_bounds_target,
+        pin_gmax_lowest_id_tie, pin_closed_loop_trace, pin_pending_when_full, pin_parameter_delay,
         pin_changes_within_one_epoch, pin_invalid_changes,
         pin_invariants]
 
@@ -368,6 +417,9 @@ MUTANTS = {
                            "Lp = self.lat[self.load(moved, gmax)]"),
     "rebalance_tie_ignores_load": ("tie = (self.load(phi, j), j, i)", "tie = (j, i)"),
     "gmax_min": ("key=lambda g: (-lat_of[g], g)", "key=lambda g: (lat_of[g], g)"),
+    "gmax_highest_id_tie": ("key=lambda g: (-lat_of[g], g)", "key=lambda g: (-lat_of[g], -g)"),
+    "scale_out_may_shrink": ("return max(self.target(n_req), m_prev)", "return self.target(n_req)"),
+    "scale_in_may_grow": ("return min(self.target(n_req), m_prev)", "return self.target(n_req)"),
     "assign_tie_more_loaded": ("key = (self.bottleneck(trial, gpus), n, g)",
                                "key = (self.bottleneck(trial, gpus), -n, g)"),
     "assign_ignores_latency": ("key = (self.bottleneck(trial, gpus), n, g)", "key = (n, g)"),

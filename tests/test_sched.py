@@ -170,6 +170,21 @@ def test_hand_derived_closed_loop_trace():
     assert groups() == {1: [3, 4], 3: [2, 5], 4: [1]}
 
 
+def test_hand_derived_scale_direction_and_gmax_tie():
+    """The oracle's hand-derived traces of the scale-out bound (imbalanced (4,0,0) placement that
+    migration cannot fix, rho_max 1.0 above the band, proportional target 2 < M = 3: M stays 3)
+    and of the lowest-id g_max among tied bottleneck GPUs ((3,3,1): session 1 of g0 moves to g2),
+    on the library and the oracle side by side."""
+    A = lambda *ids: [(SR.ARRIVE, i, 0) for i in ids]  # noqa: E731
+    E = lambda k, *ids: [(k, i, 0) for i in ids]       # noqa: E731
+    lib, ref = pair(4, 1, 3, 3, LAT4, 1.0, alpha=1e6)
+    run_both(lib, ref, [A(*range(1, 13)), E(SR.DEPART, 2, 5, 8, 11, 3, 6, 9, 12)])
+    assert lib.gpu_loads() == [(0, 4), (1, 0), (2, 0)]
+    lib, ref = pair(4, 3, 3, 3, LAT4, 1.0)
+    run_both(lib, ref, [A(*range(1, 10)), E(SR.DEPART, 3, 9)])
+    assert dict(lib.placement())[1] == 2 and dict(lib.placement())[2] == 1
+
+
 def test_pending_and_infinite_load_signal():
     lib = sched.Scheduler(2, 1, 1, 1, [0.0, 100.0, 150.0], 1.0)
     d = lib.step([(SR.ARRIVE, i, 0) for i in (1, 2, 3)])
