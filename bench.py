@@ -105,6 +105,29 @@ def cpu_baseline(w, q, k, v, o_gpu, seconds):
     }, {"rows": int(done), "max_abs": float(err.max()), "mean_abs": float(err.mean())}
 
 
+def input_rounding(w, o_gpu):
+    """Reported, not gated: the error of the GPU output (computed from the inputs rounded once to
+    bf16) against the fp64 oracle on those bf16 inputs -- the kernel's own error -- and against
+    the oracle on the unrounded fp32 draws, which adds the effect of rounding the inputs."""
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from oracle import ts_ref
+
+    out = {}
+    for name, (q, k, v) in (("oracle_on_bf16_inputs", W.make_inputs(w)),
+                            ("oracle_on_fp32_inputs", W.make_inputs_f32(w))):
+        if q.dtype == torch.bfloat16:
+            ref = ts_ref.attn_full(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), w.cu_seqlens,
+                                   w.scale)
+        else:
+            ref = ts_ref.attn_full(*(x.double().numpy() for x in (q, k, v)), w.cu_seqlens, w.scale)
+        err = np.abs(o_gpu.astype(np.float64).reshape(ref.shape) - ref)
+        out[name] = {"max_abs": float(err.max()), "mean_abs": float(err.mean())}
+    return out
+
+
 def gemm_reference(torch, dev, n=16384, reps=4):
     """Context only: the bf16 rate of a plain n^3 matrix product by torch.matmul (hipBLASLt)
     on the same device and run, timed after the attention.  MI355X runs these MFMA-bound loads
@@ -410,6 +433,8 @@ def main():
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic},
     }
+    if w.name == "tiny":
+        result["config"]["input_rounding"] = input_rounding(w, out.float().cpu().numpy())
     if not args.no_cpu_baseline:
         o_host = out.float().cpu().numpy()
         del qd, kd, vd

@@ -661,15 +661,19 @@ __device__ __forceinline__ void write_result(const Item& it, const Out& out,
     const int64_t slab = (int64_t)out.split * out.tq;  // first row of this split's slab
     const uint32_t o_bytes = ((uint32_t)(it.q_len - 1) * (uint32_t)H + 1) * D * 4;
     __amdgpu_buffer_rsrc_t rpo = make_rsrc(out.part_o + ((slab + it.q_start) * H + it.h) * D, o_bytes);
+    // Byte offsets of fp32 rows reach twice the bf16 ones: with (q_len + 256) * H * D * 2 < 2^31
+    // (the host's size limit) and qrow < q_len + 256 they stay below 2^32, so they are formed in
+    // unsigned 32-bit arithmetic (the buffer offset register is unsigned) without wrapping.
+    const uint32_t row_off = (uint32_t)qrow * (uint32_t)(H * D) * 4u;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         f32x4 x = {oacc[db][4 * g4] * inv, oacc[db][4 * g4 + 1] * inv, oacc[db][4 * g4 + 2] * inv,
                    oacc[db][4 * g4 + 3] * inv};
-        const int ch = 32 * db + 8 * g4 + 4 * hb;
+        const uint32_t ch = 32 * db + 8 * g4 + 4 * hb;
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), rpo,
-                                               (qrow * H * D + ch) * 4, 0, 0);
+                                               __builtin_bit_cast(int, row_off + ch * 4u), 0, 0);
       }
     if (hb == 0) {
       __amdgpu_buffer_rsrc_t rl = make_rsrc(out.part_lse + (slab + it.q_start) * H + it.h, lse_bytes);

@@ -5,12 +5,26 @@ by the target of this work).  Because outputs of long segments are small (their 
 sqrt(e / L), ~0.01 at L = 32760), an absolute bar alone is weak there, so a relative Frobenius bar
 is added: the kernel rounds P to bf16 (relative 2^-9 per weight, unbiased) and the output to bf16
 (relative <= 2^-9), which puts the expected relative error near 2e-3; the bar is 1e-2.
+
+Sampled rows of the full-size workloads also pass two per-row bars (assert_rows), which a wrong
+result confined to a few rows or a few (wave, lane) slots cannot hide under:
+  * row-relative: ||o_r - ref_r|| / ||ref_r|| <= 1e-2 for every sampled row r.  The two roundings
+    above give a relative error near 2^-9 / sqrt(3) ~ 1.1e-3 each (RMS) on any row, uniform or
+    peaked, so the bar leaves a factor of five;
+  * ulp-aware per element: |o - ref| <= ulp_bf16(ref) + 1e-2 * rms(ref_r).  The output rounding
+    contributes at most half an ulp of the result; the rounding of the weights contributes an
+    error proportional to the row's scale (the term 1e-2 rms), independently of how small the
+    single element is.  The fraction of elements equal to bf16(ref) -- the correctly rounded
+    result -- is reported beside it.
 """
 import numpy as np
+import torch
 
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 REL_FRO = 1e-2
+ROW_REL = 1e-2
+ULP_FLOOR = 1e-2
 
 
 def errors(got, ref):
@@ -31,4 +45,44 @@ def assert_parity(got, ref, what=""):
     assert e["max_abs"] <= MAX_ABS, "%s: %r" % (what, e)
     assert e["mean_abs"] <= MEAN_ABS, "%s: %r" % (what, e)
     assert e["rel_fro"] <= REL_FRO, "%s: %r" % (what, e)
+    return e
+
+
+def ulp_bf16(x):
+    """The spacing of bfloat16 numbers (8 significant bits) at |x|; 0 for x = 0."""
+    m, e = np.frexp(np.abs(np.asarray(x, dtype=np.float64)))  # |x| = m 2^e, m in [0.5, 1)
+    return np.where(m == 0, 0.0, np.ldexp(1.0, e - 8))
+
+
+def bf16_of(x):
+    """x rounded to bfloat16 (to nearest even), as float64."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+    return t.to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def row_errors(got, ref):
+    """Per-row figures of sampled rows got, ref [nrows, d]."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    diff = np.abs(got - ref)
+    nrm = np.linalg.norm(ref, axis=1)
+    rel = np.linalg.norm(got - ref, axis=1) / np.maximum(nrm, 1e-300)
+    rms = nrm / np.sqrt(max(ref.shape[1], 1))
+    slack = diff / (ulp_bf16(ref) + ULP_FLOOR * rms[:, None])
+    return {
+        "row_rel_max": float(rel.max()) if rel.size else 0.0,
+        "row_rel_mean": float(rel.mean()) if rel.size else 0.0,
+        "ulp_slack_max": float(slack.max()) if slack.size else 0.0,  # <= 1 passes
+        "frac_correctly_rounded": float(np.mean(got == bf16_of(ref))) if got.size else 1.0,
+        "rows": int(ref.shape[0]),
+    }
+
+
+def assert_rows(got, ref, what=""):
+    """assert_parity plus the per-row bars of the module docstring; returns both figures."""
+    e = assert_parity(got, ref, what)
+    r = row_errors(got, ref)
+    assert r["row_rel_max"] <= ROW_REL, "%s: %r" % (what, r)
+    assert r["ulp_slack_max"] <= 1.0, "%s: %r" % (what, r)
+    e.update(r)
     return e

@@ -14,7 +14,7 @@ import pytest
 import torch
 
 import workloads as W
-from metrics import assert_parity
+from metrics import assert_parity, assert_rows
 from oracle import ts_ref
 
 pytestmark = pytest.mark.gpu
@@ -189,7 +189,7 @@ def test_kv_workload_sampled(name, n_random):
     ro, rlse = ts_ref.attn_kv_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), w.cu_q, w.cu_k,
                                    w.scale, row_t, row_h)
     got = as_f64(o[torch.from_numpy(row_t), torch.from_numpy(row_h.astype(np.int64))])
-    e = assert_parity(got, ro, name)
+    e = assert_rows(got, ro, name)
     le = check_lse(lse[torch.from_numpy(row_t), torch.from_numpy(row_h.astype(np.int64))], rlse, name)
     say(name, "errors", e, "lse", le)
     assert float(np.abs(got).mean()) > 1e-3  # not an all-zero output
@@ -276,3 +276,48 @@ def test_empty_batches_are_no_ops():
     o, lse = ts.ts_attn_fwd_kvcache(e, e, e, cu, cu, 0, 0, return_lse=True)
     assert o.shape == (0, H, d) and lse.shape == (0, H)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+def test_kv_split_call_at_the_byte_limit_sampled(splits):
+    """A query segment at the largest size the ABI accepts, (max_seqlen_q + 256) * H * d * 2 <
+    2^31 bytes, with the key range split three ways: the float32 partial results of such a
+    segment span up to 2^32 bytes, so their in-segment offsets use the whole unsigned 32-bit
+    range of the buffer stores (rows near the segment's end, last head).  Sampled rows of O and
+    lse against the oracle; one query more is refused on the host."""
+    H, d = 128, 128
+    row_bytes = H * d * 2
+    Lq = (1 << 31) // row_bytes - 256 - 1          # 65279
+    lq, lk = [Lq, 500], [2000, 3000]
+    Tq, Tk = sum(lq), sum(lk)
+    assert (Lq + 256) * row_bytes < (1 << 31) and (Lq + 256) * H * d * 4 >= (1 << 31)
+    say("kv byte limit", "Lq=%d Tq=%d Tk=%d H=%d splits=%d" % (Lq, Tq, Tk, H, splits))
+    q = W.make_device_inputs(Tq, H, d, seed=31, device=torch.device("cuda"))[0]
+    torch.cuda.empty_cache()
+    k, v = W.make_device_inputs(Tk, H, d, seed=32, device=torch.device("cuda"))[1:]
+    cq_np = np.array([0, Lq, Tq], dtype=np.int32)
+    ck_np = np.array([0, lk[0], Tk], dtype=np.int32)
+    cq, ck = torch.from_numpy(cq_np).cuda(), torch.from_numpy(ck_np).cuda()
+    scale = W.Workload("x", (1,), H, d, 0).scale
+    o, lse = ts.ts_attn_fwd_kvcache(q, k, v, cq, ck, Lq, max(lk), return_lse=True,
+                                    num_splits=splits)
+    torch.cuda.synchronize()
+    with pytest.raises(ts.TsAttnError):
+        ts.ts_attn_fwd_kvcache(q, k, v, torch.tensor([0, Lq + 1, Tq], dtype=torch.int32,
+                                                     device="cuda"), ck, Lq + 1, max(lk),
+                               num_splits=splits)
+    rng = np.random.default_rng(6)
+    row_t = np.concatenate([[0, Lq - 1, Lq - 2, Lq - 255, Lq - 256, Lq, Tq - 1],
+                            rng.integers(Lq - 3000, Lq, 40), rng.integers(0, Tq, 20)]).astype(np.int64)
+    row_h = np.concatenate([[0, H - 1, H - 2, H - 1, H - 1, H - 1, H - 1],
+                            rng.integers(H - 8, H, 40), rng.integers(0, H, 20)]).astype(np.int64)
+    tt, hh = torch.from_numpy(row_t).cuda(), torch.from_numpy(row_h).cuda()
+    got, got_lse = o[tt, hh].cpu(), lse[tt, hh].cpu()
+    del o, lse
+    hq, hk, hv = (W.bf16_bits(x.cpu()) for x in (q, k, v))
+    del q, k, v
+    torch.cuda.empty_cache()
+    ro, rlse = ts_ref.attn_kv_rows(hq, hk, hv, cq_np, ck_np, scale, row_t, row_h.astype(np.int32))
+    e = assert_rows(as_f64(got), ro, "kv byte limit")
+    le = check_lse(got_lse, rlse, "kv byte limit")
+    say("kv byte limit errors", e, "lse", le)

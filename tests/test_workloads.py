@@ -46,7 +46,7 @@ def test_workload_table():
 
 def test_sample_rows_cover_segment_ends_for_every_head():
     w = W.WORKLOADS["varlen_serving"]
-    rt, rh = W.sample_rows(w)
+    rt, rh = W.sample_rows(w, full_tiles=False)
     assert rt.size == rh.size == w.H * 6 * 66
     cu = w.cu_seqlens
     for h in range(w.H):
@@ -54,8 +54,29 @@ def test_sample_rows_cover_segment_ends_for_every_head():
         for s in range(6):
             assert cu[s] in ts and cu[s + 1] - 1 in ts
     assert rt.min() >= 0 and rt.max() < w.T
-    rt2, _ = W.sample_rows(w)
+    rt2, _ = W.sample_rows(w, full_tiles=False)
     assert np.array_equal(rt, rt2)
+
+
+@pytest.mark.parametrize("name", ["dit_small", "dit_large", "highres", "varlen_serving"])
+def test_sample_rows_reach_every_tile_slot_and_differ_per_head(name):
+    """Every (wave, lane) slot of a 256-query tile is sampled in every segment that has it, the
+    random rows differ between heads, and one complete tile plus the ragged last tile of every
+    segment are included whole."""
+    w = W.WORKLOADS[name]
+    rt, rh = W.sample_rows(w)
+    cu = w.cu_seqlens
+    seg = np.searchsorted(cu, rt, side="right") - 1
+    for s in range(len(w.seqlens)):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        sel = seg == s
+        assert set(((rt[sel] - lo) % 256).tolist()) == set(range(min(256, hi - lo)))
+        assert set(range(256 * ((hi - lo) // 256) + lo, hi)) <= set(rt[sel].tolist())
+        t0 = [t for t in range(lo, hi - 255, 256) if set(range(t, t + 256)) <= set(rt[sel].tolist())]
+        assert t0, (name, s)
+    a, b = set(rt[rh == 0].tolist()), set(rt[rh == 1].tolist())
+    assert len(a ^ b) > 100
+    assert rt.min() >= 0 and rt.max() < w.T and rh.max() < w.H
 
 
 def test_kv_workloads_shapes_and_draws():

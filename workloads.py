@@ -70,8 +70,26 @@ WORKLOADS = {
                         note="21x45x80 latent, L=75600, H=40, d=128"),
     "varlen_serving": Workload("varlen_serving", (8190, 8190, 16380, 32760, 32760, 2730), 12,
                                128, 5, note="6 packed sessions, T=101010, H=12, d=128"),
+    # head width 64 at scale: the dit_small latent with the same model width split into twice
+    # the heads (24 x 64 = 12 x 128), so the flops equal dit_small's and the exponentials per
+    # flop double
+    "dit_small_d64": Workload("dit_small_d64", (32760,), 24, 64, 8, True,
+                              note="21x30x52 latent, L=32760, H=24, d=64"),
 }
 ORDER = ["tiny", "dit_small", "dit_large", "highres", "varlen_serving"]
+
+
+def make_inputs_f32(w, seed=None):
+    """(q, k, v) float32 CPU tensors [T, H, d]: the draws of make_inputs before their rounding
+    to bf16."""
+    g = torch.Generator().manual_seed(w.seed if seed is None else seed)
+    shape = (w.T, w.H, w.d)
+    q = torch.randn(shape, generator=g, dtype=torch.float32)
+    k = torch.randn(shape, generator=g, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, dtype=torch.float32)
+    if w.k_offset:
+        k += torch.randn((w.H, w.d), generator=g, dtype=torch.float32) * float(np.sqrt(2.0))
+    return q, k, v
 
 
 def make_inputs(w, seed=None):
@@ -167,20 +185,55 @@ def make_kv_inputs(w, seed=None):
     return q, k, v
 
 
-def sample_kv_rows(w, n_random=64, seed=None):
-    """(row_t, row_h) over the query rows: for every head, the first and last query of every
-    segment with queries plus n_random seeded random ones (seed 100 + workload seed)."""
-    rng = np.random.default_rng(100 + w.seed if seed is None else seed)
-    cu = w.cu_q
-    ts = []
-    for s in range(len(w.q_seqlens)):
+QUERY_TILE = 256  # queries per work item of the attention kernels: 8 waves x 32 lanes
+
+
+def _stratified_rows(cu, H, n_random, rng, full_tiles):
+    """(row_t, row_h) over the rows [cu[s], cu[s+1]) of every segment s and every head h:
+      * the first and the last row of the segment;
+      * n_random rows drawn independently per (segment, head), stratified over the position
+        inside a QUERY_TILE-row tile: head h of segment s takes the residues
+        (o_s + n_random h + i) mod QUERY_TILE, i < n_random (o_s a random offset per segment),
+        each at a random tile that holds it, so every (wave, lane) slot of a tile is checked
+        once QUERY_TILE / n_random heads are sampled;
+      * if full_tiles: every row of one random complete tile (at a random head) and every row
+        of the segment's ragged last tile (at another random head)."""
+    ts, hs = [], []
+    for s in range(len(cu) - 1):
         lo, hi = int(cu[s]), int(cu[s + 1])
-        if hi <= lo:
+        L = hi - lo
+        if L <= 0:
             continue
-        ts.extend([lo, hi - 1])
-        ts.extend(rng.integers(lo, hi, size=n_random).tolist())
-    ts = np.asarray(ts, dtype=np.int64)
-    return np.tile(ts, w.H), np.repeat(np.arange(w.H, dtype=np.int32), ts.size)
+        off = int(rng.integers(QUERY_TILE))
+        for h in range(H):
+            rows = [lo, hi - 1]
+            for i in range(n_random):
+                r = (off + n_random * h + i) % QUERY_TILE
+                if r < L:
+                    n_tiles = (L - r + QUERY_TILE - 1) // QUERY_TILE  # tiles whose slot r exists
+                    rows.append(lo + QUERY_TILE * int(rng.integers(n_tiles)) + r)
+                else:
+                    rows.append(int(rng.integers(lo, hi)))
+            ts.extend(rows)
+            hs.extend([h] * len(rows))
+        if full_tiles:
+            whole = L // QUERY_TILE
+            if whole:
+                t0 = lo + QUERY_TILE * int(rng.integers(whole))
+                ts.extend(range(t0, t0 + QUERY_TILE))
+                hs.extend([int(rng.integers(H))] * QUERY_TILE)
+            if L % QUERY_TILE:
+                t0 = lo + QUERY_TILE * whole
+                ts.extend(range(t0, hi))
+                hs.extend([int(rng.integers(H))] * (hi - t0))
+    return np.asarray(ts, dtype=np.int64), np.asarray(hs, dtype=np.int32)
+
+
+def sample_kv_rows(w, n_random=64, seed=None, full_tiles=True):
+    """(row_t, row_h) over the query rows of a chunk-vs-cache workload, as sample_rows does for
+    the segments of cu_q (seed 100 + workload seed)."""
+    rng = np.random.default_rng(100 + w.seed if seed is None else seed)
+    return _stratified_rows(w.cu_q, w.H, n_random, rng, full_tiles)
 
 
 def bf16_bits(t):
@@ -192,22 +245,13 @@ def sha256(t):
     return hashlib.sha256(bf16_bits(t).tobytes()).hexdigest()
 
 
-def sample_rows(w, n_random=64, seed=None):
+def sample_rows(w, n_random=64, seed=None, full_tiles=True):
     """(row_t, row_h): for every head, the first and last token of every non-empty segment plus
-    n_random seeded random tokens per segment (seed 100 + workload seed)."""
+    n_random tokens per segment stratified over the slots of a query tile, and (full_tiles) a
+    complete tile and the ragged last tile of every segment; seed 100 + workload seed.  See
+    _stratified_rows."""
     rng = np.random.default_rng(100 + w.seed if seed is None else seed)
-    cu = w.cu_seqlens
-    ts = []
-    for s in range(len(w.seqlens)):
-        lo, hi = int(cu[s]), int(cu[s + 1])
-        if hi <= lo:
-            continue
-        ts.extend([lo, hi - 1])
-        ts.extend(rng.integers(lo, hi, size=n_random).tolist())
-    ts = np.asarray(ts, dtype=np.int64)
-    row_t = np.tile(ts, w.H)
-    row_h = np.repeat(np.arange(w.H, dtype=np.int32), ts.size)
-    return row_t, row_h
+    return _stratified_rows(w.cu_seqlens, w.H, n_random, rng, full_tiles)
 
 
 # ---- session event traces for the closed-loop scheduler ------------------------------------
