@@ -44,6 +44,8 @@
  *    capturing stream: the first two take their plan buffer from a stream-ordered memory pool,
  *    and the copy looks up where its operands live.  So does any call that would be the first
  *    on its device, since the one-time device set-up must run outside capture.
+ *    ts_attn_fwd_kvcache_noalloc allocates nothing and is not refused (after the device's
+ *    first call).
  *  - Size limits: (L or max_seqlen + 256) * H * d * 2 bytes must stay below 2^31, and the
  *    work items (H * ceil(L / 256) per sequence; H * (ceil(T / 256) + nseq) for packed
  *    batches; 16 * H * (ceil(total_q / 256) + nseq) for chunk-vs-cache calls) below 2^23.
@@ -58,7 +60,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 4
+#define TS_ATTN_ABI_VERSION 5
 
 typedef enum ts_status {
   TS_OK = 0,
@@ -73,7 +75,8 @@ typedef enum ts_status {
   TS_ERR_NOMEM = 9,       /* device scratch allocation failed */
   TS_ERR_SEGMENTS = 10,   /* cu_seqlens contents invalid (reported only in validation mode) */
   TS_ERR_MEMORY = 11,     /* a copy operand is neither current-device memory nor pinned host memory */
-  TS_ERR_CAPTURE = 12     /* the call cannot be recorded into a HIP graph (see "Graph capture") */
+  TS_ERR_CAPTURE = 12,    /* the call cannot be recorded into a HIP graph (see "Graph capture") */
+  TS_ERR_SCRATCH = 13     /* the call needs more than the static scratch of ts_attn_fwd_kvcache_noalloc */
 } ts_status;
 
 /*
@@ -145,6 +148,33 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                         int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
                         int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits,
                         void* stream);
+
+/*
+ * The chunk-vs-cache call of ts_attn_fwd_kvcache without any device memory allocation, for
+ * callers that cannot allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Arguments, result and errors are those of ts_attn_fwd_kvcache, except:
+ *  - Scratch: the plan and the split partials live in one static device array of 32 MiB per
+ *    device (allocated when the library's code is loaded on that device, held until the process
+ *    ends), not in a per-call allocation.  A call needs
+ *      align256(4 * (2 nseq + 2)) + [n > 1] (align256(4 n total_q H) + 4 n total_q H d)
+ *    bytes for n key ranges.  A forced num_splits whose partials do not fit returns
+ *    TS_ERR_SCRATCH before any HIP call; num_splits = 0 takes the library's choice, lowered to
+ *    the largest n that fits (n = 1 always fits).
+ *  - Races: every call on a device shares that device's array, and a call leaves its contents
+ *    behind.  Calls on one stream are ordered; calls that may overlap on one device (different
+ *    streams, or host threads without ordering between their streams) race on the array and give
+ *    unspecified results.  Nothing in the array needs to start at zero: each call writes every
+ *    entry it later reads.
+ *  - Graph capture: allowed once the device has been set up by an earlier call of any entry
+ *    point (the device's first call returns TS_ERR_CAPTURE on a capturing stream).
+ *  - TS_ATTN_VALIDATE is ignored: invalid offsets always make the call a device-side no-op.
+ * With the same split count n the result equals ts_attn_fwd_kvcache's bit for bit.
+ */
+int ts_attn_fwd_kvcache_noalloc(const void* q, const void* k, const void* v, void* o, float* lse,
+                                const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                                int32_t nseq, int32_t max_seqlen_q, int32_t max_seqlen_k,
+                                int32_t total_q, int32_t total_k, int32_t H, int32_t d,
+                                float scale, int32_t num_splits, void* stream);
 
 /*
  * Session-state copy: suspend (device -> host), resume (host -> device) and compaction (device

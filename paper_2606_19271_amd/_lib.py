@@ -7,7 +7,8 @@ from .build import LIB
 TS_OK = 0
 STATUS_NAMES = ["TS_OK", "TS_ERR_NULL", "TS_ERR_SHAPE", "TS_ERR_HEAD_DIM", "TS_ERR_SCALE",
                 "TS_ERR_ALIGN", "TS_ERR_ALIAS", "TS_ERR_UNSUPPORTED", "TS_ERR_HIP",
-                "TS_ERR_NOMEM", "TS_ERR_SEGMENTS", "TS_ERR_MEMORY", "TS_ERR_CAPTURE"]
+                "TS_ERR_NOMEM", "TS_ERR_SEGMENTS", "TS_ERR_MEMORY", "TS_ERR_CAPTURE",
+                "TS_ERR_SCRATCH"]
 globals().update({name: i for i, name in enumerate(STATUS_NAMES)})
 
 _lib = None
@@ -36,6 +37,8 @@ def load():
     lib.ts_attn_fwd_varlen.restype = ctypes.c_int
     lib.ts_attn_fwd_kvcache.argtypes = [p, p, p, p, p, p, p] + [i32] * 7 + [f32, i32, p]
     lib.ts_attn_fwd_kvcache.restype = ctypes.c_int
+    lib.ts_attn_fwd_kvcache_noalloc.argtypes = lib.ts_attn_fwd_kvcache.argtypes
+    lib.ts_attn_fwd_kvcache_noalloc.restype = ctypes.c_int
     i64 = ctypes.c_int64
     lib.ts_state_copy.argtypes = [p, i64, p, i64, p, i32, p]
     lib.ts_state_copy.restype = ctypes.c_int

@@ -1,5 +1,5 @@
-"""Torch-facing binding of the C ABI (ts_attn_fwd, ts_attn_fwd_varlen, ts_attn_fwd_kvcache):
-argument marshalling only.
+"""Torch-facing binding of the C ABI (ts_attn_fwd, ts_attn_fwd_varlen, ts_attn_fwd_kvcache,
+ts_attn_fwd_kvcache_noalloc): argument marshalling only.
 
 Every step of the computation runs in libts_attn.so on the tensors' device and on torch's current
 stream of that device; nothing here computes attention, and there is no fallback path.
@@ -100,6 +100,21 @@ def ts_attn_fwd_kvcache(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_s
     scores) when return_lse is set or an lse tensor is passed.  num_splits: 0 lets the library
     choose, 1..16 forces that many key ranges per query tile (merged by their log-sum-exp).
     """
+    return _kvcache("ts_attn_fwd_kvcache", q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q,
+                    max_seqlen_k, scale, out, lse, return_lse, num_splits)
+
+
+def ts_attn_fwd_kvcache_noalloc(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_seqlen_k,
+                                scale=None, out=None, lse=None, return_lse=False, num_splits=0):
+    """ts_attn_fwd_kvcache without any device allocation inside the library: its scratch is a
+    static 32 MiB array per device, shared by every call on that device (calls that overlap on
+    one device race).  Pass `out` (and `lse`) to allocate nothing on the torch side either."""
+    return _kvcache("ts_attn_fwd_kvcache_noalloc", q, k, v, cu_seqlens_q, cu_seqlens_k,
+                    max_seqlen_q, max_seqlen_k, scale, out, lse, return_lse, num_splits)
+
+
+def _kvcache(entry, q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_seqlen_k, scale, out,
+             lse, return_lse, num_splits):
     for name, t in (("q", q), ("k", k), ("v", v)):
         _check_tensor(name, t, 3)
     if (k.shape != v.shape or k.shape[1:] != q.shape[1:] or k.device != q.device
@@ -127,13 +142,13 @@ def ts_attn_fwd_kvcache(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_s
     lib = _lib.load()
     with torch.cuda.device(q.device):
         stream = torch.cuda.current_stream(q.device).cuda_stream
-        rc = lib.ts_attn_fwd_kvcache(_ptr(q), _ptr(k), _ptr(v), _ptr(out),
-                                     _ptr(lse) if lse is not None else ctypes.c_void_p(None),
-                                     _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
-                                     _lib.i32("nseq", cu_seqlens_q.numel() - 1),
-                                     _lib.i32("max_seqlen_q", max_seqlen_q),
-                                     _lib.i32("max_seqlen_k", max_seqlen_k), _lib.i32("Tq", Tq),
-                                     _lib.i32("Tk", Tk), _lib.i32("H", H), _lib.i32("d", d), s,
-                                     _lib.i32("num_splits", num_splits), ctypes.c_void_p(stream))
+        rc = getattr(lib, entry)(_ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                 _ptr(lse) if lse is not None else ctypes.c_void_p(None),
+                                 _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
+                                 _lib.i32("nseq", cu_seqlens_q.numel() - 1),
+                                 _lib.i32("max_seqlen_q", max_seqlen_q),
+                                 _lib.i32("max_seqlen_k", max_seqlen_k), _lib.i32("Tq", Tq),
+                                 _lib.i32("Tk", Tk), _lib.i32("H", H), _lib.i32("d", d), s,
+                                 _lib.i32("num_splits", num_splits), ctypes.c_void_p(stream))
     _lib.check(rc)
     return (out, lse) if lse is not None else out

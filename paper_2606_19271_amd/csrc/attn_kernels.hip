@@ -948,6 +948,16 @@ hipError_t configure_kernels() {
   return hipSuccess;
 }
 
+// Scratch of the allocation-free chunk call: its plan and, for split calls, the float32 partial
+// results, in one array per device that lives as long as the loaded library.  Host code never
+// passes `scratch` itself to a kernel (on the host the name is only a stand-in for the device
+// symbol); it looks up the device address once per device and passes that.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_address(void** ptr) {
+  return hipGetSymbolAddress(ptr, HIP_SYMBOL(scratch));
+}
+
 hipError_t launch_dense(const DenseArgs& a, hipStream_t st) {
   return a.d == 64 ? launch_dense_d<64>(a, st) : launch_dense_d<128>(a, st);
 }

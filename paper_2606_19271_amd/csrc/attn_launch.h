@@ -40,6 +40,9 @@ struct PackedArgs {
 constexpr int kQueryTile = 256;             // queries per work item of the attention kernels
 constexpr int kMergeThreads = 256;          // threads per workgroup of the merge kernel
 constexpr int64_t kCopyChunkBytes = 32768;  // bytes copied by one state-copy workgroup
+// Bytes of the static device scratch array of the allocation-free chunk call (plan and split
+// partials), one per device, held from the library's load until the process ends.
+constexpr int64_t kScratchBytes = (int64_t)32 << 20;
 
 // Upper bound of the number of work items of a packed batch (its launch grid).
 int64_t packed_grid_bound(int32_t total_q, int32_t nseq, int32_t H, int32_t n_split);
@@ -65,6 +68,8 @@ hipError_t launch_state_copy(const void* src, void* dst, const CopyList& list, b
                              bool dst_host, hipStream_t st);
 
 hipError_t configure_kernels();
+// Device address of the current device's copy of the static scratch array (kScratchBytes).
+hipError_t scratch_address(void** ptr);
 hipError_t launch_dense(const DenseArgs& a, hipStream_t st);
 hipError_t launch_packed(const PackedArgs& a, hipStream_t st);
 

@@ -24,33 +24,57 @@ struct DeviceState {
   std::once_flag once;
   std::atomic<bool> set_up{false};  // init_device has run (whatever its outcome)
   int status = TS_ERR_UNSUPPORTED;  // TS_OK once the device is known to be usable
+  int dev = -1;
   int xcd_chunk = 32;
   int cus = 256;
-  hipMemPool_t pool = nullptr;
+  void* scratch = nullptr;          // this device's copy of the static scratch array
+  std::once_flag pool_once;         // the pool is made by the first call that allocates
+  hipMemPool_t pool = nullptr;      // null if its creation failed
 };
 
 DeviceState g_dev[kMaxDevices];
 
+// One-time set-up of a device, with that device current: architecture, kernel attributes and the
+// device address of the static scratch array (each device holds its own copy of the array).
 void init_device(int dev, DeviceState* st) {
   hipDeviceProp_t p;
+  st->dev = dev;
   if (hipGetDeviceProperties(&p, dev) != hipSuccess) { st->status = TS_ERR_HIP; return; }
   if (strncmp(p.gcnArchName, "gfx950", 6) != 0) { st->status = TS_ERR_UNSUPPORTED; return; }
   // gfx950: 8 XCDs; one 512-thread workgroup resides per CU.
   st->xcd_chunk = p.multiProcessorCount / 8 > 0 ? p.multiProcessorCount / 8 : 1;
   st->cus = p.multiProcessorCount;
   if (tsattn::configure_kernels() != hipSuccess) { st->status = TS_ERR_HIP; return; }
-  hipMemPoolProps props;
-  memset(&props, 0, sizeof props);
-  props.allocType = hipMemAllocationTypePinned;
-  props.location.type = hipMemLocationTypeDevice;
-  props.location.id = dev;
-  if (hipMemPoolCreate(&st->pool, &props) != hipSuccess) { st->status = TS_ERR_HIP; return; }
-  uint64_t keep = UINT64_MAX;  // keep freed plan buffers in the pool between calls
-  if (hipMemPoolSetAttribute(st->pool, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) {
+  void* ptr = nullptr;
+  if (tsattn::scratch_address(&ptr) != hipSuccess || ptr == nullptr) {
+    (void)hipGetLastError();
     st->status = TS_ERR_HIP;
     return;
   }
+  st->scratch = ptr;
   st->status = TS_OK;
+}
+
+// The device's stream-ordered memory pool for the plan buffers of the allocating calls, created
+// on first use (never under capture: those calls refuse a capturing stream before this).
+hipMemPool_t device_pool(DeviceState* st) {
+  std::call_once(st->pool_once, [st] {
+    hipMemPoolProps props;
+    memset(&props, 0, sizeof props);
+    props.allocType = hipMemAllocationTypePinned;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = st->dev;
+    hipMemPool_t pool = nullptr;
+    if (hipMemPoolCreate(&pool, &props) != hipSuccess) { (void)hipGetLastError(); return; }
+    uint64_t keep = UINT64_MAX;  // keep freed plan buffers in the pool between calls
+    if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipMemPoolDestroy(pool);
+      return;
+    }
+    st->pool = pool;
+  });
+  return st->pool;
 }
 
 // Whether stream s is recording a HIP graph.  A failed query (which leaves an error behind that
@@ -172,23 +196,38 @@ int32_t auto_splits(int cus, int32_t total_q, int32_t max_k, int32_t H) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Plan buffer (and split workspace) from the device's pool, the launches, the optional
-// validation read-back, and the stream-ordered release.
-int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
-  const size_t plan_bytes = align256((size_t)tsattn::plan_ints(a.nseq) * sizeof(int32_t));
-  size_t bytes = plan_bytes;
-  size_t lse_bytes = 0;
-  if (a.n_split > 1) {
-    lse_bytes = align256((size_t)a.n_split * a.total_q * a.H * sizeof(float));
-    bytes += lse_bytes + (size_t)a.n_split * a.total_q * a.H * a.d * sizeof(float);
+// Bytes of device scratch a packed call needs: the plan and, with n > 1 key ranges, the float32
+// partial lse [n][tq][H] and O [n][tq][H][d], each part 256-byte aligned.
+int64_t scratch_bytes(int32_t nseq, int32_t n, int32_t tq, int32_t H, int32_t d) {
+  int64_t b = (int64_t)align256((size_t)tsattn::plan_ints(nseq) * sizeof(int32_t));
+  if (n > 1) {
+    b += (int64_t)align256((size_t)n * tq * H * sizeof(float));
+    b += (int64_t)n * tq * H * d * (int64_t)sizeof(float);
   }
-  char* buf = nullptr;
-  if (hipMallocFromPoolAsync((void**)&buf, bytes, st->pool, s) != hipSuccess) return TS_ERR_NOMEM;
+  return b;
+}
+
+// Points a.plan (and, for a split call, a.part_lse / a.part_o) into buf, laid out as in
+// scratch_bytes.
+void carve(tsattn::PackedArgs& a, char* buf) {
+  const size_t plan_bytes = align256((size_t)tsattn::plan_ints(a.nseq) * sizeof(int32_t));
   a.plan = (int32_t*)buf;
   if (a.n_split > 1) {
+    const size_t lse_bytes = align256((size_t)a.n_split * a.total_q * a.H * sizeof(float));
     a.part_lse = (float*)(buf + plan_bytes);
     a.part_o = (float*)(buf + plan_bytes + lse_bytes);
   }
+}
+
+// Plan buffer (and split workspace) from the device's pool, the launches, the optional
+// validation read-back, and the stream-ordered release.
+int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
+  hipMemPool_t pool = device_pool(st);
+  if (!pool) return TS_ERR_NOMEM;
+  const size_t bytes = (size_t)scratch_bytes(a.nseq, a.n_split, a.total_q, a.H, a.d);
+  char* buf = nullptr;
+  if (hipMallocFromPoolAsync((void**)&buf, bytes, pool, s) != hipSuccess) return TS_ERR_NOMEM;
+  carve(a, buf);
   int rc = tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
   if (rc == TS_OK && validate_mode()) {
     int32_t head[2] = {0, 0};
@@ -200,6 +239,20 @@ int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
   }
   if (hipFreeAsync(buf, s) != hipSuccess && rc == TS_OK) rc = TS_ERR_HIP;
   return rc;
+}
+
+// Checks shared by both chunk-vs-cache entry points (everything but the stream and the memory).
+int check_kvcache_call(const void* q, const void* k, const void* v, const void* o,
+                       const float* lse, const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                       int32_t nseq, int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
+                       int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits) {
+  if (!cu_seqlens_q || !cu_seqlens_k) return TS_ERR_NULL;
+  if (nseq < 0 || num_splits < 0 || num_splits > kMaxSplits) return TS_ERR_SHAPE;
+  int rc = check_kv(q, k, v, o, lse, total_q, total_k, max_seqlen_q, max_seqlen_k, H, d, scale);
+  if (rc != TS_OK) return rc;
+  if (tsattn::packed_grid_bound(total_q, nseq, H, kMaxSplits) >= kGridLimit) return TS_ERR_SHAPE;
+  if (tsattn::merge_blocks(total_q, H, d) >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
+  return TS_OK;
 }
 
 // Device-visible address of a copy operand: device memory of the current device, or pinned
@@ -247,6 +300,7 @@ const char* ts_attn_status_str(int status) {
     case TS_ERR_SEGMENTS: return "TS_ERR_SEGMENTS: invalid cu_seqlens contents";
     case TS_ERR_MEMORY: return "TS_ERR_MEMORY: pointer is neither device memory of the current device nor pinned host memory";
     case TS_ERR_CAPTURE: return "TS_ERR_CAPTURE: this call cannot be recorded into a HIP graph (packed and copy calls, or a device's first call)";
+    case TS_ERR_SCRATCH: return "TS_ERR_SCRATCH: the call needs more device scratch than the allocation-free entry point holds";
     default: return "unknown ts_status";
   }
 }
@@ -287,12 +341,9 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                         int32_t max_seqlen_q, int32_t max_seqlen_k, int32_t total_q,
                         int32_t total_k, int32_t H, int32_t d, float scale, int32_t num_splits,
                         void* stream) {
-  if (!cu_seqlens_q || !cu_seqlens_k) return TS_ERR_NULL;
-  if (nseq < 0 || num_splits < 0 || num_splits > kMaxSplits) return TS_ERR_SHAPE;
-  int rc = check_kv(q, k, v, o, lse, total_q, total_k, max_seqlen_q, max_seqlen_k, H, d, scale);
+  int rc = check_kvcache_call(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
+                              max_seqlen_k, total_q, total_k, H, d, scale, num_splits);
   if (rc != TS_OK) return rc;
-  if (tsattn::packed_grid_bound(total_q, nseq, H, kMaxSplits) >= kGridLimit) return TS_ERR_SHAPE;
-  if (tsattn::merge_blocks(total_q, H, d) >= ((int64_t)1 << 31)) return TS_ERR_SHAPE;
   if (nseq == 0 || total_q == 0) return TS_OK;
   if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
   DeviceState* st = current_device(&rc, (hipStream_t)stream);
@@ -302,6 +353,32 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                        max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
   return run_packed(st, a, (hipStream_t)stream);
+}
+
+int ts_attn_fwd_kvcache_noalloc(const void* q, const void* k, const void* v, void* o, float* lse,
+                                const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                                int32_t nseq, int32_t max_seqlen_q, int32_t max_seqlen_k,
+                                int32_t total_q, int32_t total_k, int32_t H, int32_t d,
+                                float scale, int32_t num_splits, void* stream) {
+  int rc = check_kvcache_call(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
+                              max_seqlen_k, total_q, total_k, H, d, scale, num_splits);
+  if (rc != TS_OK) return rc;
+  if (nseq == 0 || total_q == 0) return TS_OK;
+  // a forced split count is checked against the scratch before the device is touched
+  if (scratch_bytes(nseq, num_splits > 0 ? num_splits : 1, total_q, H, d) > tsattn::kScratchBytes)
+    return TS_ERR_SCRATCH;
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);
+  if (!st) return rc;
+  int32_t n = num_splits;
+  if (n == 0) {  // the library's choice, lowered until its partial results fit the scratch
+    n = auto_splits(st->cus, total_q, max_seqlen_k, H);
+    while (n > 1 && scratch_bytes(nseq, n, total_q, H, d) > tsattn::kScratchBytes) --n;
+  }
+  tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
+                       max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
+                       nullptr, nullptr, nullptr};
+  carve(a, (char*)st->scratch);
+  return tsattn::launch_packed(a, (hipStream_t)stream) == hipSuccess ? TS_OK : TS_ERR_HIP;
 }
 
 int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_bytes,

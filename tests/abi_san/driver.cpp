@@ -20,7 +20,7 @@ namespace {
 int g_fail = 0;
 int64_t g_calls = 0;
 
-bool known_status(int s) { return s >= TS_OK && s <= TS_ERR_CAPTURE; }
+bool known_status(int s) { return s >= TS_OK && s <= TS_ERR_SCRATCH; }
 
 void expect(bool cond, const char* what, long long a, long long b, long long c) {
   if (!cond) {
@@ -106,9 +106,22 @@ int main() {
                 ++g_calls;
                 expect(known_status(s), "kv status", nseq, mq, H);
                 if (ns < 0 || ns > 16) expect(s != TS_OK, "bad splits accepted", nseq, ns, H);
+                const int s2 = ts_attn_fwd_kvcache_noalloc(q, k, v, o, (ns & 1) ? lse : nullptr, cu, cu,
+                                                           nseq, mq, mk, tq, tk, H, 128, 0.1f, ns,
+                                                           nullptr);
+                ++g_calls;
+                expect(known_status(s2), "kv noalloc status", nseq, mq, H);
+                // the same checks, plus the scratch bound of a forced split count
+                expect(s2 == s || s2 == TS_ERR_SCRATCH, "kv noalloc differs", nseq, tq, ns);
               }
   expect(ts_attn_fwd_kvcache(q, k, v, o, static_cast<float*>(fake((6ull << 44) + 2)), cu, cu, 1, 64, 64, 64, 64, 2, 64, 1.0f, 0, nullptr) ==
              TS_ERR_ALIGN, "misaligned lse", 0, 0, 0);
+  // allocation-free chunk call: 2 splits of 32768 query rows at H = 2, d = 128 need 64 MiB of
+  // partials, more than its 32 MiB scratch; 4096 rows (8 MiB) fit
+  expect(ts_attn_fwd_kvcache_noalloc(q, k, v, o, nullptr, cu, cu, 1, 32768, 64, 32768, 64, 2, 128, 1.0f, 2, nullptr) ==
+             TS_ERR_SCRATCH, "noalloc scratch bound", 0, 0, 0);
+  expect(ts_attn_fwd_kvcache_noalloc(nullptr, nullptr, nullptr, nullptr, nullptr, cu, cu, 1, 0, 0, 0, 0, 2, 64, 1.0f, 0, nullptr) == TS_OK,
+         "noalloc empty chunk", 0, 0, 0);
 
   // state copy: ranges with extreme offsets and sizes, extreme buffer sizes
   const int64_t I64MAX = std::numeric_limits<int64_t>::max();

@@ -11,6 +11,11 @@ namespace tsattn {
 
 hipError_t configure_kernels() { return hipErrorNotSupported; }
 
+hipError_t scratch_address(void**) {
+  std::fprintf(stderr, "scratch_address reached in the host-only build\n");
+  std::abort();
+}
+
 hipError_t launch_dense(const DenseArgs&, hipStream_t) {
   std::fprintf(stderr, "launch_dense reached in the host-only build\n");
   std::abort();

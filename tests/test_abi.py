@@ -35,7 +35,7 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
     assert names == ["ts_attn_abi_version", "ts_attn_fwd", "ts_attn_fwd_kvcache",
-                     "ts_attn_fwd_varlen", "ts_attn_status_str"]
+                     "ts_attn_fwd_kvcache_noalloc", "ts_attn_fwd_varlen", "ts_attn_status_str"]
     copy_names = sorted(set(re.findall(r"\b(ts_state_\w+)\s*\(",
                                        re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S))))
     assert copy_names == ["ts_state_copy"]
@@ -145,10 +145,30 @@ def test_varlen_argument_checks(lib):
 
 
 def kvcache(lib, q=A, k=A, v=A, o=BIG, lse=None, cuq=A, cuk=A, nseq=2, max_q=64, max_k=256,
-            tq=128, tk=512, H=2, d=128, scale=0.125, splits=0):
+            tq=128, tk=512, H=2, d=128, scale=0.125, splits=0, entry="ts_attn_fwd_kvcache"):
     P = ctypes.c_void_p
-    return lib.ts_attn_fwd_kvcache(P(q), P(k), P(v), P(o), P(lse), P(cuq), P(cuk), nseq, max_q,
-                                   max_k, tq, tk, H, d, scale, splits, P(None))
+    return getattr(lib, entry)(P(q), P(k), P(v), P(o), P(lse), P(cuq), P(cuk), nseq, max_q,
+                               max_k, tq, tk, H, d, scale, splits, P(None))
+
+
+def test_kvcache_noalloc_argument_checks(lib):
+    """The allocation-free chunk call makes every check of ts_attn_fwd_kvcache, and refuses a
+    forced split count whose partial results exceed its 32 MiB scratch before any HIP call."""
+    def noalloc(**kw):
+        return kvcache(lib, entry="ts_attn_fwd_kvcache_noalloc", **kw)
+    assert noalloc(cuk=0) == _lib.TS_ERR_NULL
+    assert noalloc(splits=17) == _lib.TS_ERR_SHAPE
+    assert noalloc(d=96) == _lib.TS_ERR_HEAD_DIM
+    assert noalloc(scale=math.nan) == _lib.TS_ERR_SCALE
+    assert noalloc(o=A + 300 * 2 * 128 * 2) == _lib.TS_ERR_ALIAS
+    assert noalloc(nseq=0) == _lib.TS_OK and noalloc(tq=0) == _lib.TS_OK
+    # plan (256 B) + lse (align256(4 n tq H)) + partial O (4 n tq H d) against 32 MiB
+    tq, H, d = 8192, 2, 128
+    assert 256 + 4 * 3 * tq * H + 4 * 3 * tq * H * d <= 32 << 20 < 256 + 4 * 4 * tq * H + 4 * 4 * tq * H * d
+    big = BIG * 4
+    assert noalloc(tq=tq, max_q=tq, o=big, splits=4) == _lib.TS_ERR_SCRATCH
+    assert noalloc(tq=tq, max_q=tq, o=big, splits=16) == _lib.TS_ERR_SCRATCH
+    assert noalloc(tq=tq, max_q=tq, o=big, splits=4, d=80) == _lib.TS_ERR_HEAD_DIM  # checks first
 
 
 def test_kvcache_argument_checks(lib):
