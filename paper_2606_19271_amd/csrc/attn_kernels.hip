@@ -130,6 +130,18 @@ struct Item {
   int ntiles;       // key tiles of the item
 };
 
+// Query tiles per (sequence, head) kept in the main item order of a dense call: all nq, unless the
+// last tile is ragged enough to leave a wave without queries.  Such a tile's workgroup runs its
+// phases faster than its neighbours (its idle waves skip their compute), so the items after it
+// on its CU would drift out of step with the items that stream the same keys and values on the
+// same XCD, and lose their shared L2 hits; these tiles are run after all full ones instead.
+// (Packed and chunk calls keep their per-segment order: there the ragged tiles share their key
+// ranges with the segment's other tiles, and moving them away from those costs more L2 hits.)
+__host__ __device__ inline int main_query_tiles(int len) {
+  const int nq = (len + kBM - 1) / kBM, tail = len % kBM;
+  return tail != 0 && (tail + 31) / 32 < kWaves ? nq - 1 : nq;
+}
+
 // Where the results of an item go.  kFinal: O as bf16 [Tq][H][D] and, when lse is not null,
 // the natural log-sum-exp of every row as float [Tq][H].  kPartial (one key range of a split
 // call): the normalised O of that range as float [splits][Tq][H][D] and its log-sum-exp as
@@ -710,15 +722,25 @@ template <int D>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                   const __bf16* __restrict__ v, __bf16* __restrict__ o, int L, int H, int nq,
-                  int total, int chunk, float c, int negate_q) {
+                  int nfull, int total, int chunk, float c, int negate_q) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int item = remap_block(blockIdx.x, total, chunk);
-  const int bh = item / nq;
+  // items [0, main): query tiles 0 .. nfull - 1 of every (sequence, head), head-major; then, when
+  // nfull < nq, the last query tile of every (sequence, head)
+  const int n_main = total - (nq - nfull) * (total / nq);
+  int bh, qt;
+  if (item < n_main) {
+    bh = item / nfull;
+    qt = item % nfull;
+  } else {
+    bh = item - n_main;
+    qt = nq - 1;
+  }
   Item it;
   it.q_start = it.k_start = (int64_t)(bh / H) * L;
   it.q_len = it.k_len = L;
   it.h = bh % H;
-  it.q_begin = (item % nq) * kBM;
+  it.q_begin = qt * kBM;
   it.tile_begin = 0;
   it.ntiles = (L + kBN - 1) / kBN;
   Out out{o, nullptr, nullptr, nullptr, 0, 0};
@@ -894,7 +916,8 @@ static hipError_t launch_dense_d(const DenseArgs& a, hipStream_t st) {
   const float c = fabsf(a.scale) * kLog2e;
   hipLaunchKernelGGL((attn_dense_kernel<D>), dim3(total), dim3(kThreads), Geo<D>::kLds, st,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
-                     a.L, a.H, nq, total, a.xcd_chunk, c, a.scale < 0.0f ? 1 : 0);
+                     a.L, a.H, nq, main_query_tiles(a.L), total, a.xcd_chunk, c,
+                     a.scale < 0.0f ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -100,6 +100,23 @@ def test_dense_batch_full(d):
 
 
 @pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("L", [1, 100, 224, 225, 256, 480, 513, 737])
+def test_dense_ragged_lengths_full(L, d):
+    """The dense call runs the ragged last query tile of every (sequence, head) after all full
+    tiles when that tile leaves a wave without queries (L mod 256 in 1..224): every such order,
+    and the plain one (225, 256, 480), against the oracle and bitwise against the packed call."""
+    B, H = 3, 2
+    w, q, k, v = draw([L] * B, H, d, seed=3000 + L + d)
+    say("dense ragged", B, L, H, d)
+    o = ts.ts_attn_fwd(q.cuda().view(B, L, H, d), k.cuda().view(B, L, H, d),
+                       v.cuda().view(B, L, H, d))
+    torch.cuda.synchronize()
+    o = o.cpu().view(B * L, H, d)
+    assert_parity(as_f64(o), oracle_full(q, k, v, [L] * B, w.scale), "dense L=%d d=%d" % (L, d))
+    assert torch.equal(o.view(torch.int16), run_varlen(q, k, v, [L] * B).view(torch.int16))
+
+
+@pytest.mark.parametrize("d", [64, 128])
 def test_varlen_with_empty_and_tiny_segments_full(d):
     seqlens = [0, 5, 0, 300, 1, 0, 129, 64, 2, 513, 0]
     w, q, k, v = draw(seqlens, 2, d, seed=5 + d)
