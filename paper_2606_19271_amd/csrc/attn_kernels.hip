@@ -20,7 +20,7 @@
 //    issues the softmax VALU work, and they swap roles at each workgroup barrier.  On gfx950
 //    v_exp_f32 shares the VALU pipe with the other vector ops, while MFMAs run in the matrix
 //    core, so the softmax can hide under the other wave's matrix work.
-//  * K and V tiles of 64 keys are staged in LDS in rings of four (K) and three (V), laid out
+//  * K and V tiles of 64 keys (128 at d = 64) are staged in LDS in rings of four (K) and three (V), laid out
 //    (K padded, V XOR-swizzled) so that the MFMA operand reads are free of bank conflicts.  They
 //    arrive by LDS DMA (buffer_load ... lds), which needs no registers and no LDS write
 //    instructions, issued only in the vector steps; the raw buffer descriptor's range check
@@ -60,7 +60,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 
 constexpr int kBM = kQueryTile;  // queries per work item
-constexpr int kBN = 64;        // keys per K/V tile
 constexpr int kWaves = 8;      // waves per workgroup, 32 queries each
 constexpr int kThreads = kWaves * 64;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -77,6 +76,10 @@ constexpr unsigned kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format 
 //    which keeps the transposed V reads free of bank conflicts.
 template <int D>
 struct Geo {
+  // Keys per K/V tile.  A matrix step costs the same number of MFMA clocks at both head widths
+  // (32 32x32x16 MFMAs per wave): 64 keys at d = 128, 128 keys at d = 64, so the fixed costs of
+  // a step (two barriers, the DMA issue, the waits) weigh the same against its matrix work.
+  static constexpr int kBN = key_tile(D);
   static constexpr int kChunks = D / 8;                  // 16-byte chunks per row of d bf16
   static constexpr int kKRow = D * 2 + 16;               // padded K row stride (bytes)
   static constexpr int kVRow = D * 2;                    // V row stride (bytes)
@@ -176,12 +179,13 @@ __device__ __forceinline__ int remap_block(int b, int total, int chunk) {
   return full + x * q + min(x, rem) + j;
 }
 
-// S^T = K Q^T for one 64-key tile: two 32-key blocks, each an accumulation over d in steps of 16.
-// Accumulator register r of block kb holds key 32*kb + 8*(r/4) + 4*hb + r%4 of the tile for the
-// lane's query (lane & 31).  The two blocks' MFMAs alternate, so that each Q fragment is the B
-// operand of two consecutive MFMAs: under the power cap an operand held over consecutive MFMAs
-// costs less switching energy, and the clock rises accordingly (measured +0.6 %).  MFMA i uses
-// the K fragment (kk, kb) = (i / 2, i % 2); the first kPreReads of them were read ahead into kp.
+// S^T = K Q^T for one key tile: 32-key blocks (two at d = 128, four at d = 64), each an
+// accumulation over d in steps of 16.  Accumulator register r of block kb holds key
+// 32*kb + 8*(r/4) + 4*hb + r%4 of the tile for the lane's query (lane & 31).  The blocks' MFMAs
+// alternate, so that each Q fragment is the B operand of consecutive MFMAs: under the power cap
+// an operand held over consecutive MFMAs costs less switching energy, and the clock rises
+// accordingly (measured +0.6 % for two).  MFMA i uses the K fragment (kk, kb) = (i / nkb, i % nkb)
+// with nkb blocks per tile; the first kPreReads of them were read ahead into kp.
 constexpr int kPreReads = 8;
 
 template <int D>
@@ -194,22 +198,24 @@ __device__ __forceinline__ const lds_char* k_frag(const lds_char* kt, int kk, in
 template <int D>
 __device__ __forceinline__ void k_preread(const lds_char* __restrict__ kt, bf16x8 (&kp)[kPreReads],
                                           int lane) {
+  constexpr int kKB = Geo<D>::kBN / 32;  // 32-key blocks per tile
 #pragma unroll
   for (int i = 0; i < kPreReads; ++i)
-    kp[i] = *(const lds_bf16x8*)k_frag<D>(kt, i / 2, i % 2, lane);
+    kp[i] = *(const lds_bf16x8*)k_frag<D>(kt, i / kKB, i % kKB, lane);
 }
 
 template <int D>
 __device__ __forceinline__ void qk_tile(const lds_char* __restrict__ kt, const bf16x8 (&qf)[D / 16],
-                                        const bf16x8 (&kp)[kPreReads], f32x16 (&s)[kBN / 32],
-                                        int lane) {
+                                        const bf16x8 (&kp)[kPreReads],
+                                        f32x16 (&s)[Geo<D>::kBN / 32], int lane) {
+  constexpr int kKB = Geo<D>::kBN / 32;
 #pragma unroll
-  for (int kb = 0; kb < kBN / 32; ++kb) s[kb] = f32x16{};
+  for (int kb = 0; kb < kKB; ++kb) s[kb] = f32x16{};
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb) {
-      const int i = 2 * kk + kb;
+    for (int kb = 0; kb < kKB; ++kb) {
+      const int i = kKB * kk + kb;
       bf16x8 a = i < kPreReads ? kp[i] : *(const lds_bf16x8*)k_frag<D>(kt, kk, kb, lane);
       s[kb] = mfma32(a, qf[kk], s[kb]);
     }
@@ -260,9 +266,10 @@ __device__ __forceinline__ bf16x8 row_sum_selector(int lane) {
 // The row sums of one tile's weights, on two accumulators in turn: switching the matrix core
 // between the 32x32x16 and the 16x16x32 shape costs about 6 clocks each way (measured), so the
 // four row-sum MFMAs are issued together, and two chains keep them from waiting on each other.
-__device__ __forceinline__ void row_sums(bf16x8 sel, const bf16x8 (&p)[kBN / 16], f32x4 (&l)[2]) {
+template <int NT>
+__device__ __forceinline__ void row_sums(bf16x8 sel, const bf16x8 (&p)[NT], f32x4 (&l)[2]) {
 #pragma unroll
-  for (int t = 0; t < kBN / 16; ++t)
+  for (int t = 0; t < NT; ++t)
     l[t & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, p[t], l[t & 1], 0, 0, 0);
 }
 
@@ -272,10 +279,10 @@ __device__ __forceinline__ void row_sums(bf16x8 sel, const bf16x8 (&p)[kBN / 16]
 // 16t + 4hb + 0..3, elements 4-7 from rows 16t + 8 + 4hb + 0..3.
 template <int D>
 __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const VOffsets<D>& vo,
-                                        const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32]) {
+                                        const bf16x8 (&p)[Geo<D>::kBN / 16], f32x16 (&o)[D / 32]) {
   using G = Geo<D>;
 #pragma unroll
-  for (int t = 0; t < kBN / 16; ++t)
+  for (int t = 0; t < G::kBN / 16; ++t)
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       const lds_char* base = vt + 16 * t * G::kVRow;
@@ -290,12 +297,12 @@ __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const V
 // product.  Returns the bitwise OR of the packed words: bit 14 of a bf16 is the top bit of its
 // exponent, set exactly when the (non-negative) value is at least 2 or not finite, so
 // (OR & 0x40004000) != 0 flags a tile whose weights are not all below 2.
-template <bool kMasked>
-__device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
+template <int NT, bool kMasked>
+__device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[NT / 2], bf16x8 (&p)[NT],
                                              float m_c, float c, int keys_valid, int hb) {
   unsigned any = 0;
 #pragma unroll
-  for (int t = 0; t < kBN / 16; ++t) {
+  for (int t = 0; t < NT; ++t) {
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
       float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
@@ -333,12 +340,14 @@ __device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[kBN / 32], bf16x8
 constexpr float kBias = 39.0f;
 
 template <int D, bool kMasked>
-__device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[kBN / 16],
-                                             float& m_c, f32x16 (&o)[D / 32], f32x4 (&l)[2], float c,
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[Geo<D>::kBN / 32],
+                                             bf16x8 (&p)[Geo<D>::kBN / 16], float& m_c,
+                                             f32x16 (&o)[D / 32], f32x4 (&l)[2], float c,
                                              int keys_valid, int lane) {
+  constexpr int kBN = Geo<D>::kBN;
   const int hb = lane >> 5;
   if (!kMasked) {
-    const unsigned any = exp_pack<false>(s, p, m_c, c, kBN, hb);
+    const unsigned any = exp_pack<kBN / 16, false>(s, p, m_c, c, kBN, hb);
     if (__builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) == 0) return;
   }
   if (kMasked) {
@@ -366,7 +375,7 @@ __device__ __forceinline__ void softmax_tile(f32x16 (&s)[kBN / 32], bf16x8 (&p)[
     for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
   l[0] *= alpha;
   l[1] *= alpha;
-  exp_pack<kMasked>(s, p, m_c, c, keys_valid, hb);
+  exp_pack<kBN / 16, kMasked>(s, p, m_c, c, keys_valid, hb);
 }
 
 // Lane offsets (bytes, relative to the tile's first row in global memory) of one wave's share
@@ -446,6 +455,7 @@ __device__ __forceinline__ void block_sync() {
 // requested kPreReads MFMAs earlier (one b128 read per S MFMA, two transpose reads per PV MFMA).
 template <int D, bool kPV>
 __device__ __forceinline__ constexpr int m_step_reads(int i) {
+  constexpr int kBN = Geo<D>::kBN;
   constexpr int kRS = kPV ? kBN / 16 : 0;  // row-sum MFMAs
   constexpr int kQK = (kBN / 32) * (D / 16);
   if (i < kRS) return 0;
@@ -456,9 +466,11 @@ __device__ __forceinline__ constexpr int m_step_reads(int i) {
 template <int D, bool kPV>
 __device__ __forceinline__ void m_step(const lds_char* __restrict__ kt, const lds_char* __restrict__ vt,
                                        const VOffsets<D>& vo, const bf16x8 (&qf)[D / 16],
-                                       const bf16x8 (&kp)[kPreReads], f32x16 (&s)[kBN / 32],
-                                       const bf16x8 (&p)[kBN / 16], f32x16 (&o)[D / 32],
+                                       const bf16x8 (&kp)[kPreReads],
+                                       f32x16 (&s)[Geo<D>::kBN / 32],
+                                       const bf16x8 (&p)[Geo<D>::kBN / 16], f32x16 (&o)[D / 32],
                                        bf16x8 sel, f32x4 (&l)[2], int lane) {
+  constexpr int kBN = Geo<D>::kBN;
   if (kPV) row_sums(sel, p, l);
   qk_tile<D>(kt, qf, kp, s, lane);
   if (kPV) pv_tile<D>(vt, vo, p, o);
@@ -513,6 +525,7 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
                                                const __bf16* __restrict__ v, const Out& out,
                                                int H, float c, bool negate_q, char* smem) {
   using G = Geo<D>;
+  constexpr int kBN = G::kBN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int gw = wave & (G::kGroupWaves - 1);  // wave inside its group
@@ -742,7 +755,7 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
   it.h = bh % H;
   it.q_begin = qt * kBM;
   it.tile_begin = 0;
-  it.ntiles = (L + kBN - 1) / kBN;
+  it.ntiles = (L + Geo<D>::kBN - 1) / Geo<D>::kBN;
   Out out{o, nullptr, nullptr, nullptr, 0, 0};
   run_item<D, kFinal>(it, q, k, v, out, H, c, negate_q != 0, smem);
 }
@@ -781,7 +794,7 @@ attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
   it.h = local / per_head;
   const int split = (local % per_head) / nq;
   it.q_begin = (local % nq) * kBM;
-  const int seg_tiles = (it.k_len + kBN - 1) / kBN;
+  const int seg_tiles = (it.k_len + Geo<D>::kBN - 1) / Geo<D>::kBN;
   const int per_split = (seg_tiles + n_split - 1) / n_split;
   it.tile_begin = split * per_split;
   it.ntiles = max(0, min(per_split, seg_tiles - it.tile_begin));

@@ -39,6 +39,8 @@ struct PackedArgs {
 // Sizes shared by the kernels and the host-side planning (attn_plan.cpp).
 constexpr int kQueryTile = 256;             // queries per work item of the attention kernels
 constexpr int kMergeThreads = 256;          // threads per workgroup of the merge kernel
+// Keys per K/V tile of the attention kernels at head width d (64 or 128).
+constexpr int key_tile(int d) { return d == 64 ? 128 : 64; }
 constexpr int64_t kCopyChunkBytes = 32768;  // bytes copied by one state-copy workgroup
 // Bytes of the static device scratch array of the allocation-free chunk call (plan and split
 // partials), one per device, held from the library's load until the process ends.

@@ -180,9 +180,10 @@ int check_kv(const void* q, const void* k, const void* v, const void* o, const f
 // one item's key tiles.  Query tiles that already fill the GPU are not split (the partials would
 // only add traffic); otherwise n minimises rounds(items * n) * ceil(tiles / n), the smallest n
 // winning ties, with at least 4 key tiles per range.
-int32_t auto_splits(int cus, int32_t total_q, int32_t max_k, int32_t H) {
-  const int64_t items = (int64_t)H * ((total_q + 255) / 256);
-  const int64_t tiles = ((int64_t)max_k + 63) / 64;
+int32_t auto_splits(int cus, int32_t total_q, int32_t max_k, int32_t H, int32_t d) {
+  const int64_t items = (int64_t)H * ((total_q + tsattn::kQueryTile - 1) / tsattn::kQueryTile);
+  const int64_t kt = tsattn::key_tile(d);
+  const int64_t tiles = ((int64_t)max_k + kt - 1) / kt;
   if (items <= 0 || items >= cus || tiles < 8) return 1;
   int32_t best = 1;
   int64_t best_cost = INT64_MAX;
@@ -348,7 +349,7 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
   if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
   DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
-  const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H);
+  const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H, d);
   tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
                        max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
@@ -371,7 +372,7 @@ int ts_attn_fwd_kvcache_noalloc(const void* q, const void* k, const void* v, voi
   if (!st) return rc;
   int32_t n = num_splits;
   if (n == 0) {  // the library's choice, lowered until its partial results fit the scratch
-    n = auto_splits(st->cus, total_q, max_seqlen_k, H);
+    n = auto_splits(st->cus, total_q, max_seqlen_k, H, d);
     while (n > 1 && scratch_bytes(nseq, n, total_q, H, d) > tsattn::kScratchBytes) --n;
   }
   tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,

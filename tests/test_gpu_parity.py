@@ -235,7 +235,8 @@ def test_score_jump_mid_sequence(gap):
 
 # ------------------------------------------------------------------------- full-size workloads
 
-@pytest.mark.parametrize("name", ["dit_small", "dit_large", "highres", "varlen_serving"])
+@pytest.mark.parametrize("name", ["dit_small", "dit_large", "highres", "varlen_serving",
+                                  "dit_small_d64"])
 def test_workload_sampled(name):
     w = W.WORKLOADS[name]
     say("workload", name, "T=%d H=%d d=%d" % (w.T, w.H, w.d))
