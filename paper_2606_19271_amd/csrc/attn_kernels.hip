@@ -548,8 +548,13 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   else dma_offsets_v<D>(gw, lane, row_bytes, voff);
   // this group's fetch of the item's tile j: K_j (group A) into stage j % 4, V_j (group B) into
   // stage vstage, which the caller keeps equal to j % 3
+  // Fetches run up to kFetchAhead tiles past the item's last one (into stages nobody reads).
+  // Their tile index stops at the segment's end, where every row reads as zero: then no byte
+  // offset exceeds (k_len + 2 kBN - 1) rows, which the host's size limit, (len + 256) rows of
+  // H * D * 2 bytes below 2^31, keeps within int range at both tile sizes.
+  const int seg_tiles = (it.k_len + kBN - 1) / kBN;
   auto fetch = [&](int j, int vstage) {
-    const int key0 = (it.tile_begin + j) * kBN;
+    const int key0 = min(it.tile_begin + j, seg_tiles) * kBN;
     if (!kGroupB) dma_k<D>(rk, key0, row_bytes, ktile(j & 3), koff, gw);
     else dma_v<D>(rv, key0, row_bytes, vtile(vstage), voff, gw);
   };

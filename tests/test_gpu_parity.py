@@ -486,13 +486,16 @@ def test_closed_form_golden_cases():
 
 # --------------------------------------------------------------------------- the size limit
 
-def test_segments_at_the_byte_limit_sampled():
+@pytest.mark.parametrize("d", [128, 64])
+def test_segments_at_the_byte_limit_sampled(d):
     """A segment at the largest size the ABI accepts, (L + 256) * H * d * 2 < 2^31 bytes, in a
     packed batch whose second segment starts beyond 2 GiB: exercises the 32-bit in-segment
-    offsets at their limit and the 64-bit segment bases (H = 128 keeps the attention cheap)."""
-    H, d = 128, 128
+    offsets at their limit (also those of the K/V fetches that run ahead past the segment's end:
+    up to three 128-key tiles at d = 64) and the 64-bit segment bases (H = 128 keeps the
+    attention cheap)."""
+    H = 128
     row_bytes = H * d * 2
-    L = (1 << 31) // row_bytes - 256 - 1          # 65279: the largest accepted segment
+    L = (1 << 31) // row_bytes - 256 - 1          # 65279 at d = 128, 130815 at d = 64
     seqlens = [L, 40000]
     T = sum(seqlens)
     assert (L + 256) * row_bytes < (1 << 31) <= (L + 257) * row_bytes
@@ -525,7 +528,7 @@ def test_segments_at_the_byte_limit_sampled():
     torch.cuda.empty_cache()
     say("oracle rows", row_t.size)
     ref = ts_ref.attn_rows(hq, hk, hv, cu_np, scale, row_t, row_h)
-    e = assert_rows(as_f64(got), ref, "byte limit")
+    e = assert_rows(as_f64(got), ref, "byte limit d=%d" % d)
     trivial = errors(np.zeros_like(ref), ref)
     say("byte limit errors", e, "zero-output errors", trivial)
     assert e["mean_abs"] < 0.1 * trivial["mean_abs"]
