@@ -72,6 +72,9 @@ def cpu_baseline(w, q, k, v, o_gpu, seconds):
         row_t, row_h = W.sample_kv_rows(w, n_random=4096, seed=999)
     else:
         row_t, row_h = W.sample_rows(w, n_random=4096, seed=999)
+    # each (token, head) row once (a small call's sample would otherwise repeat rows)
+    _, first = np.unique(row_t * w.H + row_h, return_index=True)
+    row_t, row_h = row_t[first], row_h[first]
     perm = np.random.default_rng(7).permutation(row_t.size)
     row_t, row_h = row_t[perm], row_h[perm]
     qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
