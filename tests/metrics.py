@@ -7,7 +7,8 @@ is added: the kernel rounds P to bf16 (relative 2^-9 per weight, unbiased) and t
 (relative <= 2^-9), which puts the expected relative error near 2e-3; the bar is 1e-2.
 
 Sampled rows of the full-size workloads also pass two per-row bars (assert_rows), which a wrong
-result confined to a few rows or a few (wave, lane) slots cannot hide under:
+result confined to a few rows or a few (wave, lane) slots cannot hide under (the full-tensor tests
+of short, ragged or peaked segments pass the row-relative one):
   * row-relative: ||o_r - ref_r|| / ||ref_r|| <= 1e-2 for every sampled row r.  The two roundings
     above give a relative error near 2^-9 / sqrt(3) ~ 1.1e-3 each (RMS) on any row, uniform or
     peaked, so the bar leaves a factor of five;
@@ -61,14 +62,20 @@ def bf16_of(x):
 
 
 def row_errors(got, ref):
-    """Per-row figures of sampled rows got, ref [nrows, d]."""
+    """Per-row figures of got, ref: [nrows, d], or any shape whose last axis is d (a full output
+    [T, H, d] is T * H rows).  An exact zero error counts as zero however small its bar."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
+    d = ref.shape[-1] if ref.ndim else 1
+    got, ref = got.reshape(-1, d), ref.reshape(-1, d)
     diff = np.abs(got - ref)
     nrm = np.linalg.norm(ref, axis=1)
-    rel = np.linalg.norm(got - ref, axis=1) / np.maximum(nrm, 1e-300)
-    rms = nrm / np.sqrt(max(ref.shape[1], 1))
-    slack = diff / (ulp_bf16(ref) + ULP_FLOOR * rms[:, None])
+    err = np.linalg.norm(got - ref, axis=1)
+    rel = np.where(err == 0, 0.0, err / np.maximum(nrm, 1e-300))
+    rms = nrm / np.sqrt(max(d, 1))
+    bar = ulp_bf16(ref) + ULP_FLOOR * rms[:, None]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        slack = np.where(diff == 0, 0.0, diff / bar)
     return {
         "row_rel_max": float(rel.max()) if rel.size else 0.0,
         "row_rel_mean": float(rel.mean()) if rel.size else 0.0,
@@ -78,11 +85,19 @@ def row_errors(got, ref):
     }
 
 
-def assert_rows(got, ref, what=""):
-    """assert_parity plus the per-row bars of the module docstring; returns both figures."""
+def assert_rows(got, ref, what="", elementwise=True):
+    """assert_parity plus the per-row bars of the module docstring; returns both figures.
+
+    elementwise=False keeps the row-relative bar only.  The element bar assumes the rounding error
+    of the weights scales with the row's output, as it does on the long segments of the full-size
+    workloads (thousands of comparable weights).  A short or peaked row whose output cancels
+    between a few dominant keys (V_1 ~ -V_2 in some channel) has an error that scales with the
+    spread of V over those keys instead, 2^-10 |V_1c - V_2c| for two equal weights, which can
+    exceed 1 % of the row's RMS in that channel."""
     e = assert_parity(got, ref, what)
     r = row_errors(got, ref)
     assert r["row_rel_max"] <= ROW_REL, "%s: %r" % (what, r)
-    assert r["ulp_slack_max"] <= 1.0, "%s: %r" % (what, r)
+    if elementwise:
+        assert r["ulp_slack_max"] <= 1.0, "%s: %r" % (what, r)
     e.update(r)
     return e

@@ -83,7 +83,7 @@ def test_kv_full(d):
     say("kv full", d, LQ, LK)
     o, lse = run_kv(w, q, k, v, splits=1)
     ro, rlse = oracle(w, q, k, v, w.scale)
-    e = assert_parity(as_f64(o), ro, "kv full d=%d" % d)
+    e = assert_rows(as_f64(o), ro, "kv full d=%d" % d, elementwise=False)
     le = check_lse(lse, rlse, "kv full d=%d" % d)
     say("errors", e, "lse", le)
     nokeys = slice(int(w.cu_q[2]), int(w.cu_q[3]))  # queries of the segment without keys
@@ -97,7 +97,7 @@ def test_kv_forced_splits_full(splits, d):
     say("kv splits", splits, d)
     o, lse = run_kv(w, q, k, v, splits=splits)
     ro, rlse = oracle(w, q, k, v, w.scale)
-    assert_parity(as_f64(o), ro, "kv splits=%d d=%d" % (splits, d))
+    assert_rows(as_f64(o), ro, "kv splits=%d d=%d" % (splits, d), elementwise=False)
     check_lse(lse, rlse, "kv splits=%d d=%d" % (splits, d))
     # the split result differs from the unsplit one only by the rounding of the partials
     o1, _ = run_kv(w, q, k, v, splits=1)
@@ -130,7 +130,7 @@ def test_kv_random_batches_full(seed):
     say(what)
     o, lse = run_kv(w, q, k, v, splits=splits, scale=scale)
     ro, rlse = oracle(w, q, k, v, sc)
-    assert_parity(as_f64(o), ro, what)
+    assert_rows(as_f64(o), ro, what, elementwise=False)
     check_lse(lse, rlse, what)
 
 
@@ -164,7 +164,8 @@ def test_kv_other_scales(scale):
     for splits in (1, 3):
         o, lse = run_kv(w, q, k, v, splits=splits, scale=scale)
         ro, rlse = oracle(w, q, k, v, scale)
-        assert_parity(as_f64(o), ro, "kv scale=%g splits=%d" % (scale, splits))
+        assert_rows(as_f64(o), ro, "kv scale=%g splits=%d" % (scale, splits),
+                    elementwise=False)
         check_lse(lse, rlse, "kv scale=%g splits=%d" % (scale, splits))
 
 

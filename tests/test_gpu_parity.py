@@ -70,7 +70,7 @@ def test_tiny_full_dense_and_varlen():
                              v.cuda().view(1, w.T, w.H, w.d)).view(w.T, w.H, w.d)
     torch.cuda.synchronize()
     o_var = run_varlen(q, k, v, list(w.seqlens))
-    e = assert_parity(as_f64(o_dense.cpu()), ref, "tiny dense")
+    e = assert_rows(as_f64(o_dense.cpu()), ref, "tiny dense", elementwise=False)
     say("tiny errors", e)
     assert torch.equal(o_dense.cpu().view(torch.int16), o_var.view(torch.int16))
 
@@ -82,7 +82,7 @@ def test_ragged_lengths_full(L, d):
     say("ragged", L, d)
     ref = oracle_full(q, k, v, [L], w.scale)
     o = run_varlen(q, k, v, [L])
-    assert_parity(as_f64(o), ref, "L=%d d=%d" % (L, d))
+    assert_rows(as_f64(o), ref, "L=%d d=%d" % (L, d), elementwise=False)
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -94,7 +94,8 @@ def test_dense_batch_full(d):
                        v.cuda().view(B, L, H, d))
     torch.cuda.synchronize()
     ref = oracle_full(q, k, v, [L] * B, w.scale)
-    assert_parity(as_f64(o.cpu().view(B * L, H, d)), ref, "dense batch d=%d" % d)
+    assert_rows(as_f64(o.cpu().view(B * L, H, d)), ref, "dense batch d=%d" % d,
+                elementwise=False)
     o_var = run_varlen(q, k, v, [L] * B)
     assert torch.equal(o.cpu().view(B * L, H, d).view(torch.int16), o_var.view(torch.int16))
 
@@ -112,7 +113,8 @@ def test_dense_ragged_lengths_full(L, d):
                        v.cuda().view(B, L, H, d))
     torch.cuda.synchronize()
     o = o.cpu().view(B * L, H, d)
-    assert_parity(as_f64(o), oracle_full(q, k, v, [L] * B, w.scale), "dense L=%d d=%d" % (L, d))
+    assert_rows(as_f64(o), oracle_full(q, k, v, [L] * B, w.scale), "dense L=%d d=%d" % (L, d),
+                elementwise=False)
     assert torch.equal(o.view(torch.int16), run_varlen(q, k, v, [L] * B).view(torch.int16))
 
 
@@ -123,7 +125,7 @@ def test_varlen_with_empty_and_tiny_segments_full(d):
     say("varlen empty segments", seqlens, d)
     ref = oracle_full(q, k, v, seqlens, w.scale)
     o = run_varlen(q, k, v, seqlens)
-    assert_parity(as_f64(o), ref, "varlen d=%d" % d)
+    assert_rows(as_f64(o), ref, "varlen d=%d" % d, elementwise=False)
 
 
 # lengths at and around the 64-key and 256-query tile edges, mixed with arbitrary ones
@@ -153,7 +155,8 @@ def test_random_packed_batches_full(seed):
     say("random packed", seed, lens, H, d, scale)
     ref = oracle_full(q, k, v, lens, sc)
     o = run_varlen(q, k, v, lens, scale=scale)
-    assert_parity(as_f64(o), ref, "random packed seed=%d %r H=%d d=%d scale=%r" % (seed, lens, H, d, scale))
+    assert_rows(as_f64(o), ref, "random packed seed=%d %r H=%d d=%d scale=%r" % (seed, lens, H, d, scale),
+                elementwise=False)
 
 
 def test_many_segments_beyond_sort_limit():
@@ -164,7 +167,7 @@ def test_many_segments_beyond_sort_limit():
     say("many segments", len(seqlens), sum(seqlens))
     ref = oracle_full(q, k, v, seqlens, w.scale)
     o = run_varlen(q, k, v, seqlens)
-    assert_parity(as_f64(o), ref, "5000 segments")
+    assert_rows(as_f64(o), ref, "5000 segments", elementwise=False)
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.2, 0.9])
@@ -175,7 +178,7 @@ def test_other_scales_full(scale):
     say("scale", scale)
     ref = oracle_full(q, k, v, seqlens, scale)
     o = run_varlen(q, k, v, seqlens, scale=scale)
-    assert_parity(as_f64(o), ref, "scale=%g" % scale)
+    assert_rows(as_f64(o), ref, "scale=%g" % scale, elementwise=False)
 
 
 def test_peaked_scores_full():
@@ -186,7 +189,7 @@ def test_peaked_scores_full():
     say("peaked")
     ref = oracle_full(q, k, v, seqlens, w.scale)
     o = run_varlen(q, k, v, seqlens)
-    assert_parity(as_f64(o), ref, "peaked")
+    assert_rows(as_f64(o), ref, "peaked", elementwise=False)
 
 
 def test_increasing_scores_force_rescale():
@@ -203,7 +206,7 @@ def test_increasing_scores_force_rescale():
     say("forced rescale")
     ref = oracle_full(q, k, v, [L], scale)
     o = run_varlen(q, k, v, [L])
-    assert_parity(as_f64(o), ref, "forced rescale")
+    assert_rows(as_f64(o), ref, "forced rescale", elementwise=False)
 
 
 
@@ -231,7 +234,7 @@ def test_score_jump_mid_sequence(gap):
     o = run_varlen(q, k, v, seqlens)
     got = as_f64(o)
     assert np.all(np.isfinite(got))
-    assert_parity(got, ref, "score jump %g" % gap)
+    assert_rows(got, ref, "score jump %g" % gap, elementwise=False)
 
 # ------------------------------------------------------------------------- full-size workloads
 
@@ -304,7 +307,7 @@ def test_identical_keys_give_mean_of_v():
     say("identical keys")
     o = run_varlen(q, k, v, [L])
     mean_v = v.double().mean(dim=0, keepdim=True).expand(L, H, d).numpy()
-    assert_parity(as_f64(o), mean_v, "identical keys")
+    assert_rows(as_f64(o), mean_v, "identical keys", elementwise=False)
 
 
 def test_dominant_key_returns_its_value_row():
@@ -323,8 +326,8 @@ def test_dominant_key_returns_its_value_row():
     assert float(z[jstar] - torch.cat([z[:jstar], z[jstar + 1:]]).max()) > gap
     o = run_varlen(q, k, v, [L], scale=scale)
     target = v[jstar:jstar + 1].double().expand(L, H, d).numpy()
-    assert_parity(as_f64(o), target, "dominant key")
-    assert_parity(as_f64(o), ref, "dominant key vs oracle")
+    assert_rows(as_f64(o), target, "dominant key", elementwise=False)
+    assert_rows(as_f64(o), ref, "dominant key vs oracle", elementwise=False)
 
 
 def test_constant_v_gives_constant():
@@ -335,7 +338,7 @@ def test_constant_v_gives_constant():
     v = torch.full((L, H, d), 0.71875).to(torch.bfloat16)
     say("constant V")
     o = run_varlen(q, k, v, [L])
-    assert_parity(as_f64(o), np.full((L, H, d), 0.71875), "constant V")
+    assert_rows(as_f64(o), np.full((L, H, d), 0.71875), "constant V", elementwise=False)
 
 
 # ---------------------------------------------------------------------------------- error paths
@@ -419,7 +422,7 @@ def test_runs_on_a_side_stream():
     with torch.cuda.stream(s):
         o = ts.ts_attn_fwd_varlen(qd, kd, vd, cu, w.max_seqlen)
     s.synchronize()
-    assert_parity(as_f64(o.cpu()), ref, "side stream")
+    assert_rows(as_f64(o.cpu()), ref, "side stream", elementwise=False)
 
 
 def test_concurrent_calls_from_threads_on_separate_streams():
@@ -565,7 +568,7 @@ def test_q_k_v_may_be_one_tensor():
                              x[:700].view(1, 700, 2, 128)).view(700, 2, 128)
     torch.cuda.synchronize()
     ref = oracle_full(q, q, q, seqlens, w.scale)
-    assert_parity(as_f64(o.cpu()), ref, "aliased")
+    assert_rows(as_f64(o.cpu()), ref, "aliased", elementwise=False)
     assert torch.equal(o_dense.cpu(), o[:700].cpu())
 
 

@@ -32,3 +32,17 @@ def test_row_bars_accept_rounding_and_reject_a_wrong_row():
     bad = got.copy()
     bad[3, 5] += 8 * M.ulp_bf16(ref[3, 5]) + 0.02 * np.linalg.norm(ref[3]) / 8
     assert M.row_errors(bad, ref)["ulp_slack_max"] > 1.0
+
+
+def test_row_bars_on_full_outputs_and_empty_rows():
+    # a full output [T, H, d] is T * H rows; a row whose exact result is zero (a query without
+    # keys) passes only when the output is exactly zero there
+    rng = np.random.default_rng(1)
+    ref = rng.standard_normal((5, 3, 16)) * 0.1
+    ref[2, 1] = 0.0
+    got = M.bf16_of(ref)
+    r = M.row_errors(got, ref)
+    assert r["rows"] == 15 and r["ulp_slack_max"] <= 0.5 and r["row_rel_max"] < 2.0 ** -8
+    got[2, 1, 3] = 1e-30
+    r = M.row_errors(got, ref)
+    assert r["row_rel_max"] > M.ROW_REL and r["ulp_slack_max"] > 1.0
