@@ -91,8 +91,8 @@ struct Geo {
   static constexpr int kKRing = kVStages * kVTile;       // byte offset of the K ring
   static constexpr int kLds = kKStages * kKTile + kVStages * kVTile;
   static constexpr int kGroupWaves = kWaves / 2;
-  static constexpr int kKDma = kKTile / 1024;            // DMA instructions per K tile (17 / 9)
-  static constexpr int kVDma = kVTile / 1024;            // per V tile (16 / 8)
+  static constexpr int kKDma = kKTile / 1024;            // DMA instructions per K tile (17 / 18)
+  static constexpr int kVDma = kVTile / 1024;            // per V tile (16 / 16)
   static constexpr int kKDmaMax = (kKDma + kGroupWaves - 1) / kGroupWaves;  // per wave, at most
   static constexpr int kKDmaMin = kKDma / kGroupWaves;                      // per wave, at least
   static constexpr int kVDmaPerWave = kVDma / kGroupWaves;
@@ -712,6 +712,265 @@ __device__ __forceinline__ void write_result(const Item& it, const Out& out,
   }
 }
 
+// ---- Thin items: a query tile of at most 32 queries (the ragged last tile of a segment).
+//
+// In the main schedule such a tile keeps one wave busy and seven idle for the item's whole key
+// range.  Here all eight waves share it: wave w takes the 16 queries 16 (w & 1) + 0..15 of the
+// tile and, of every K/V tile, the kBN / 64 blocks of 16 keys 16 (4 t + (w >> 1)) + 0..15, so
+// that each K/V tile is consumed by the eight waves together.  Per 16-key block a wave computes
+// S^T = K Q^T on 16x16x32 MFMAs (lane l: query l & 15, keys 4 (l >> 4) + 0..3), exponentiates
+// it with its own online maximum, and accumulates O^T += V^T P^T on 16x16x16 MFMAs, whose B
+// operand is exactly the lane's four weights and whose A operand (V^T for 16 channels, keys
+// 4 (l >> 4) + 0..3) is one transpose read.  At the end the four waves that hold the same
+// queries combine their partial (max, sum, O) through LDS, as partial results over disjoint
+// key sets: O = sum_k 2^(m_k - M) O_k / sum_k 2^(m_k - M) l_k with M = max_k m_k.
+//
+// Schedule: one barrier per K/V tile.  Waves 0-3 fetch K tiles, waves 4-7 V tiles, both two tiles
+// ahead into rings of three stages (the first three stages of the main schedule's rings); tile j
+// sits in stage j % 3.  The fetch into stage (j + 2) % 3 is issued after the barrier that closed
+// tile j - 1, the stage's last reader, and each wave waits for its fetch of tile j + 1 before the
+// barrier that closes tile j.
+constexpr int kThinQueries = 32;  // query tiles with at most this many queries take this path
+
+__device__ __forceinline__ f32x4 mfma16k32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
+                                                   __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
+}
+
+template <int D, int kMode>
+__device__ __forceinline__ void run_thin_item(const Item& it, const __bf16* __restrict__ q,
+                                              const __bf16* __restrict__ k,
+                                              const __bf16* __restrict__ v, const Out& out, int H,
+                                              float c, bool negate_q, char* smem) {
+  using G = Geo<D>;
+  constexpr int kBN = G::kBN;
+  constexpr int kSub = kBN / 64;  // 16-key blocks of a wave per K/V tile
+  constexpr int kCB = D / 16;     // 16-channel blocks of O
+  constexpr int kWait = G::kKDmaMin;
+  static_assert(G::kKDmaMin == G::kVDmaPerWave, "one wait count for both fetching groups");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool fetch_v = wave >= kWaves / 2;
+  const int gw = wave & (G::kGroupWaves - 1);
+  const int qb = wave & 1, kq = wave >> 1;
+  const int g = lane >> 4, i16 = lane & 15;
+  const int row_bytes = H * D * 2;
+  const int64_t qbase = (it.q_start * H + it.h) * D;
+  const int64_t kbase = (it.k_start * H + it.h) * D;
+  const uint32_t q_bytes = (uint32_t)(it.q_len - 1) * (uint32_t)row_bytes + D * 2;
+  const uint32_t k_bytes = (uint32_t)(it.k_len - 1) * (uint32_t)row_bytes + D * 2;
+  __amdgpu_buffer_rsrc_t rq = make_rsrc(q + qbase, q_bytes);
+  __amdgpu_buffer_rsrc_t rk = make_rsrc(k + kbase, k_bytes);
+  __amdgpu_buffer_rsrc_t rv = make_rsrc(v + kbase, k_bytes);
+  lds_char* const lds = (lds_char*)smem;
+  auto ktile = [&](int stage) { return lds + G::kKRing + stage * G::kKTile; };
+  auto vtile = [&](int stage) { return lds + G::kVRing + stage * G::kVTile; };
+  int koff[G::kKDmaMax], voff[G::kVDmaPerWave];
+  if (!fetch_v) dma_offsets_k<D>(gw, lane, row_bytes, koff);
+  else dma_offsets_v<D>(gw, lane, row_bytes, voff);
+  // as in the main schedule, fetches past the segment's end clamp their tile index there
+  const int seg_tiles = (it.k_len + kBN - 1) / kBN;
+  auto fetch = [&](int j, int stage) {
+    const int key0 = min(it.tile_begin + j, seg_tiles) * kBN;
+    if (!fetch_v) dma_k<D>(rk, key0, row_bytes, ktile(stage), koff, gw);
+    else dma_v<D>(rv, key0, row_bytes, vtile(stage), voff, gw);
+  };
+
+  // Q fragments (B operand of the 16x16x32 S MFMAs): query i16 of block qb, channels
+  // 32 kk + 8 g + 0..7
+  const int qrow = it.q_begin + 16 * qb + i16;
+  bf16x8 qf[D / 32];
+#pragma unroll
+  for (int kk = 0; kk < D / 32; ++kk) {
+    u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(rq, qrow * row_bytes + (32 * kk + 8 * g) * 2,
+                                                      0, 0);
+    if (negate_q) raw ^= u32x4{0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u};
+    qf[kk] = __builtin_bit_cast(bf16x8, raw);
+  }
+  // LDS offsets inside a tile: the K row of this lane in 16-key block t is 16 (4 t + kq) + i16;
+  // the V rows of its transpose reads are 16 (4 t + kq) + 4 g + 0..3, and the swizzle depends on
+  // the row mod 16 only, so the offset of channel block cb is the same for every block t.
+  const int krow0 = (16 * kq + i16) * G::kKRow + 16 * g;
+  const int vr16 = 4 * g + (i16 >> 2);
+  int voffs[kCB];
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb)
+    voffs[cb] = (16 * kq + vr16) * G::kVRow +
+                (((2 * cb + ((i16 & 3) >> 1)) ^ G::vswz(vr16)) << 4) + 8 * (i16 & 1);
+
+  f32x4 o[kCB];
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb) o[cb] = f32x4{};
+  float m_c = -INFINITY, l_part = 0.0f;
+  const int ntiles = it.ntiles;
+  const int last_keys = min(kBN, it.k_len - (it.tile_begin + ntiles - 1) * kBN);
+
+  fetch(0, 0);
+  fetch(1, 1);
+  wait_vmem<kWait>();
+  block_sync();
+  int st = 0;  // stage of tile j
+  for (int j = 0; j < ntiles; ++j) {
+    const int st2 = st == 0 ? 2 : st - 1;  // (j + 2) % 3
+    fetch(j + 2, st2);
+    const lds_char* kt = ktile(st);
+    const lds_char* vt = vtile(st);
+    f32x4 s[kSub];
+#pragma unroll
+    for (int t = 0; t < kSub; ++t) {
+      s[t] = f32x4{};
+#pragma unroll
+      for (int kk = 0; kk < D / 32; ++kk) {
+        const bf16x8 a = *(const lds_bf16x8*)(kt + krow0 + 64 * t * G::kKRow + 64 * kk);
+        s[t] = mfma16k32(a, qf[kk], s[t]);
+      }
+    }
+    // keys past the segment's end exist only in its last tile
+    const bool masked = j == ntiles - 1 && last_keys < kBN;
+    auto exps = [&](bf16x4 (&p)[kSub]) {
+      unsigned any = 0;
+#pragma unroll
+      for (int t = 0; t < kSub; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; r += 2) {
+          float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], c, -m_c));
+          float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r + 1], c, -m_c));
+          const int key0 = 16 * (4 * t + kq) + 4 * g + r;
+          if (masked && key0 >= last_keys) e0 = 0.0f;
+          if (masked && key0 + 1 >= last_keys) e1 = 0.0f;
+          f32x2 e = {e0, e1};
+          bf16x2 pb = __builtin_convertvector(e, bf16x2);
+          p[t][r] = pb[0];
+          p[t][r + 1] = pb[1];
+          any |= __builtin_bit_cast(unsigned, pb);
+        }
+      return any;
+    };
+    bf16x4 p[kSub];
+    const unsigned any = exps(p);
+    // as in the main schedule: the tile keeps the wave's maximum unless a weight reaches 2
+    // (first tile, a score far above the maximum so far) or keys are masked
+    if (masked || __builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) != 0) {
+      float mt = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < kSub; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = 16 * (4 * t + kq) + 4 * g + r;
+          if (!masked || key < last_keys) mt = fmaxf(mt, s[t][r]);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      // a wave can see no valid key at all in a masked tile (its blocks lie past the end);
+      // then its maximum, and everything it has accumulated, stay as they are
+      if (mt != -INFINITY) {
+        const float m_new = fmaxf(m_c, __builtin_fmaf(mt, c, kBias));
+        const float alpha = __builtin_amdgcn_exp2f(m_c - m_new);  // 0 while m_c = -inf
+        m_c = m_new;
+#pragma unroll
+        for (int cb = 0; cb < kCB; ++cb) o[cb] *= alpha;
+        l_part *= alpha;
+      }
+      exps(p);
+    }
+#pragma unroll
+    for (int t = 0; t < kSub; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) l_part += (float)p[t][r];
+#pragma unroll
+    for (int t = 0; t < kSub; ++t)
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) {
+        const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vt + 64 * t * G::kVRow + voffs[cb]));
+        o[cb] = mfma16k16(a, p[t], o[cb]);
+      }
+    wait_vmem<kWait>();
+    block_sync();
+    st = st == 2 ? 0 : st + 1;
+  }
+  wait_vmem<0>();  // the fetches past the end land before the rings are reused
+  block_sync();
+
+  // Combine the four key subsets of each query block through LDS: O_k as float
+  // [wave][16 queries][D], (m_k, l_k) as float2 [wave][16 queries] after it.
+  float l = l_part + __shfl_xor(l_part, 16);
+  l += __shfl_xor(l, 32);
+  typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
+  typedef __attribute__((address_space(3))) f32x2 lds_f32x2;
+  typedef __attribute__((address_space(3))) float lds_float;
+  lds_float* const obuf = (lds_float*)lds;
+  lds_f32x2* const mlbuf = (lds_f32x2*)(lds + kWaves * 16 * D * 4);
+  static_assert(kWaves * 16 * D * 4 + kWaves * 16 * 8 <= G::kLds, "combine buffer fits the rings");
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb)
+    *(lds_f32x4*)(obuf + (wave * 16 + i16) * D + 16 * cb + 4 * g) = o[cb];
+  if (g == 0) mlbuf[wave * 16 + i16] = f32x2{m_c, l};
+  __syncthreads();
+  // wave w now finishes queries of block qb = w & 1, channels (D / 4) (w >> 1) + (D / 16) g + ..:
+  // the waves holding block qb are qb + 2 kq2, kq2 = 0..3
+  constexpr int kCh = D / 16;  // channels per lane
+  const int ch0 = (D / 4) * kq + kCh * g;
+  float mk[4], lk[4], big = -INFINITY;
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2) {
+    const f32x2 ml = mlbuf[(qb + 2 * k2) * 16 + i16];
+    mk[k2] = ml[0];
+    lk[k2] = ml[1];
+    big = fmaxf(big, mk[k2]);
+  }
+  float acc[kCh] = {}, lsum = 0.0f;
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2) {
+    const float w = big == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mk[k2] - big);
+    lsum += w * lk[k2];
+    const lds_float* src = obuf + ((qb + 2 * k2) * 16 + i16) * D + ch0;
+#pragma unroll
+    for (int x = 0; x < kCh; x += 4) {
+      const f32x4 ov = *(const lds_f32x4*)(src + x);
+#pragma unroll
+      for (int y = 0; y < 4; ++y) acc[x + y] += w * ov[y];
+    }
+  }
+  const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+  const float lse = lsum > 0.0f ? (big + log2f(lsum)) * kLn2 : -INFINITY;
+  const uint32_t lse_bytes = ((uint32_t)(it.q_len - 1) * (uint32_t)H + 1) * 4;
+  if (kMode == kFinal) {
+    __amdgpu_buffer_rsrc_t ro = make_rsrc(out.o + qbase, q_bytes);
+#pragma unroll
+    for (int x = 0; x < kCh; x += 4) {
+      f32x4 y = {acc[x] * inv, acc[x + 1] * inv, acc[x + 2] * inv, acc[x + 3] * inv};
+      bf16x4 b = __builtin_convertvector(y, bf16x4);
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, b), ro,
+                                            qrow * row_bytes + (ch0 + x) * 2, 0, 0);
+    }
+    if (out.lse != nullptr && kq == 0 && g == 0) {
+      __amdgpu_buffer_rsrc_t rl = make_rsrc(out.lse + it.q_start * H + it.h, lse_bytes);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, qrow * H * 4, 0, 0);
+    }
+  } else {
+    const int64_t slab = (int64_t)out.split * out.tq;
+    const uint32_t o_bytes = ((uint32_t)(it.q_len - 1) * (uint32_t)H + 1) * D * 4;
+    __amdgpu_buffer_rsrc_t rpo = make_rsrc(out.part_o + ((slab + it.q_start) * H + it.h) * D, o_bytes);
+    // unsigned offsets, as in write_result
+    const uint32_t row_off = (uint32_t)qrow * (uint32_t)(H * D) * 4u;
+#pragma unroll
+    for (int x = 0; x < kCh; x += 4) {
+      f32x4 y = {acc[x] * inv, acc[x + 1] * inv, acc[x + 2] * inv, acc[x + 3] * inv};
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, y), rpo,
+                                             __builtin_bit_cast(int, row_off + (uint32_t)(ch0 + x) * 4u),
+                                             0, 0);
+    }
+    if (kq == 0 && g == 0) {
+      __amdgpu_buffer_rsrc_t rl = make_rsrc(out.part_lse + (slab + it.q_start) * H + it.h, lse_bytes);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, qrow * H * 4, 0, 0);
+    }
+  }
+}
+
 template <int D, int kMode>
 __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
                                          const __bf16* __restrict__ k, const __bf16* __restrict__ v,
@@ -724,6 +983,10 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
     for (int db = 0; db < D / 32; ++db) zero[db] = f32x16{};
     write_result<D, kMode>(it, out, zero, 0.0f, -INFINITY, H, it.q_begin + 32 * wave + (lane & 31),
                            lane >> 5);
+    return;
+  }
+  if (it.q_len - it.q_begin <= kThinQueries) {
+    run_thin_item<D, kMode>(it, q, k, v, out, H, c, negate_q, smem);
     return;
   }
   const bool active = it.q_begin + 32 * wave < it.q_len;  // some query of this wave is in range
@@ -743,7 +1006,7 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                   int nfull, int total, int chunk, float c, int negate_q) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int item = remap_block(blockIdx.x, total, chunk);
-  // items [0, main): query tiles 0 .. nfull - 1 of every (sequence, head), head-major; then, when
+  // items [0, n_main): query tiles 0 .. nfull - 1 of every (sequence, head), head-major; then, when
   // nfull < nq, the last query tile of every (sequence, head)
   const int n_main = total - (nq - nfull) * (total / nq);
   int bh, qt;

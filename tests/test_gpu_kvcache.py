@@ -104,6 +104,27 @@ def test_kv_forced_splits_full(splits, d):
     assert float((o.float() - o1.float()).abs().max()) <= 2e-2
 
 
+# Query tiles of at most 32 queries take the thin path: the eight waves share the tile, each with
+# 16 of its queries and a quarter of every key tile, and combine their partial results at the end.
+# Query tails on both sides of 16 and 32, against key counts on both sides of the 16-key blocks,
+# of a wave's quarter and of the key tile (a wave may see no key at all in the masked last tile).
+THIN_LQ = [1, 8, 16, 17, 24, 31, 32, 33, 256 + 24, 512 + 32]
+THIN_LK = [1, 15, 17, 40, 64, 129, 300, 700, 2000, 5000]
+
+
+@pytest.mark.parametrize("splits", [1, 3, 0])
+@pytest.mark.parametrize("d", [64, 128])
+def test_kv_thin_query_tiles_full(splits, d):
+    w, q, k, v = draw(THIN_LQ, THIN_LK, 3, d, 111 + d, k_offset=True)
+    what = "kv thin d=%d splits=%d" % (d, splits)
+    say(what)
+    o, lse = run_kv(w, q, k, v, splits=splits)
+    ro, rlse = oracle(w, q, k, v, w.scale)
+    e = assert_rows(as_f64(o), ro, what, elementwise=False)
+    le = check_lse(lse, rlse, what)
+    say("errors", e, "lse", le)
+
+
 @pytest.mark.parametrize("seed", range(10))
 def test_kv_random_batches_full(seed):
     # seeded random chunk batches: per segment a query count and a key count drawn independently

@@ -101,11 +101,13 @@ def test_dense_batch_full(d):
 
 
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("L", [1, 100, 224, 225, 256, 480, 513, 737])
+@pytest.mark.parametrize("L", [1, 16, 17, 100, 224, 225, 256, 280, 480, 513, 544, 737])
 def test_dense_ragged_lengths_full(L, d):
     """The dense call runs the ragged last query tile of every (sequence, head) after all full
     tiles when that tile leaves a wave without queries (L mod 256 in 1..224): every such order,
-    and the plain one (225, 256, 480), against the oracle and bitwise against the packed call."""
+    and the plain one (225, 256, 480), against the oracle and bitwise against the packed call.
+    A last tile of at most 32 queries (1, 16, 17, 280, 513, 544) takes the thin path, in which all
+    eight waves share it."""
     B, H = 3, 2
     w, q, k, v = draw([L] * B, H, d, seed=3000 + L + d)
     say("dense ragged", B, L, H, d)
