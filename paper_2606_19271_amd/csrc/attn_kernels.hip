@@ -971,7 +971,9 @@ __device__ __forceinline__ void run_thin_item(const Item& it, const __bf16* __re
   }
 }
 
-template <int D, int kMode>
+// kThin = false compiles the thin path out, for launches that have no query tile of at most
+// kThinQueries queries (the full tiles' code is then exactly that of a build without it).
+template <int D, int kMode, bool kThin = true>
 __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restrict__ q,
                                          const __bf16* __restrict__ k, const __bf16* __restrict__ v,
                                          const Out& out, int H, float c, bool negate_q, char* smem) {
@@ -985,7 +987,7 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
                            lane >> 5);
     return;
   }
-  if (it.q_len - it.q_begin <= kThinQueries) {
+  if (kThin && it.q_len - it.q_begin <= kThinQueries) {
     run_thin_item<D, kMode>(it, q, k, v, out, H, c, negate_q, smem);
     return;
   }
@@ -999,7 +1001,8 @@ __device__ __forceinline__ void run_item(const Item& it, const __bf16* __restric
   }
 }
 
-template <int D>
+// kThin: L mod kBM is in 1..kThinQueries, so the last query tile of every sequence is thin.
+template <int D, bool kThin>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                   const __bf16* __restrict__ v, __bf16* __restrict__ o, int L, int H, int nq,
@@ -1025,7 +1028,7 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
   it.tile_begin = 0;
   it.ntiles = (L + Geo<D>::kBN - 1) / Geo<D>::kBN;
   Out out{o, nullptr, nullptr, nullptr, 0, 0};
-  run_item<D, kFinal>(it, q, k, v, out, H, c, negate_q != 0, smem);
+  run_item<D, kFinal, kThin>(it, q, k, v, out, H, c, negate_q != 0, smem);
 }
 
 // Packed batch: segment s has queries [cu_q[s], cu_q[s+1]) and keys [cu_k[s], cu_k[s+1])
@@ -1195,10 +1198,12 @@ static hipError_t launch_dense_d(const DenseArgs& a, hipStream_t st) {
   const int nq = (a.L + kBM - 1) / kBM;
   const int total = a.B * a.H * nq;
   const float c = fabsf(a.scale) * kLog2e;
-  hipLaunchKernelGGL((attn_dense_kernel<D>), dim3(total), dim3(kThreads), Geo<D>::kLds, st,
-                     (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
-                     a.L, a.H, nq, main_query_tiles(a.L), total, a.xcd_chunk, c,
-                     a.scale < 0.0f ? 1 : 0);
+  const int tail = a.L % kBM;
+  auto kern = tail != 0 && tail <= kThinQueries ? attn_dense_kernel<D, true>
+                                                : attn_dense_kernel<D, false>;
+  hipLaunchKernelGGL(kern, dim3(total), dim3(kThreads), Geo<D>::kLds, st, (const __bf16*)a.q,
+                     (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o, a.L, a.H, nq,
+                     main_query_tiles(a.L), total, a.xcd_chunk, c, a.scale < 0.0f ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1234,12 +1239,15 @@ static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
 
 hipError_t configure_kernels() {
   hipError_t e;
-  e = hipFuncSetAttribute((const void*)attn_dense_kernel<64>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<64>::kLds);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)attn_dense_kernel<128>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, Geo<128>::kLds);
-  if (e != hipSuccess) return e;
+  const void* dense[4] = {(const void*)attn_dense_kernel<64, false>,
+                          (const void*)attn_dense_kernel<64, true>,
+                          (const void*)attn_dense_kernel<128, false>,
+                          (const void*)attn_dense_kernel<128, true>};
+  for (int i = 0; i < 4; ++i) {
+    e = hipFuncSetAttribute(dense[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                            i < 2 ? Geo<64>::kLds : Geo<128>::kLds);
+    if (e != hipSuccess) return e;
+  }
   const void* packed[4] = {(const void*)attn_varlen_kernel<64, kFinal>,
                            (const void*)attn_varlen_kernel<64, kPartial>,
                            (const void*)attn_varlen_kernel<128, kFinal>,
