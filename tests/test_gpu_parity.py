@@ -172,53 +172,60 @@ def test_many_segments_beyond_sort_limit():
     assert_rows(as_f64(o), ref, "5000 segments", elementwise=False)
 
 
+# Each of the special-input tests below also runs on segments whose last query tile holds at most
+# 32 queries (24, 280 = 256 + 24, 536 = 512 + 24, 1044 = 4 * 256 + 20, 1560 = 6 * 256 + 24), which
+# take the thin path: there each wave keeps its own running maximum over a quarter of every key
+# tile, and the four waves of a query block combine their partials at the end.
+@pytest.mark.parametrize("seqlens", [[200, 457], [24, 280]])
 @pytest.mark.parametrize("scale", [0.0, -0.2, 0.9])
-def test_other_scales_full(scale):
-    seqlens = [200, 457]
+def test_other_scales_full(scale, seqlens):
     w, q, k, v = draw(seqlens, 2, 128, seed=31)
     scale = float(np.float32(scale))
     say("scale", scale)
     ref = oracle_full(q, k, v, seqlens, scale)
     o = run_varlen(q, k, v, seqlens, scale=scale)
-    assert_rows(as_f64(o), ref, "scale=%g" % scale, elementwise=False)
+    assert_rows(as_f64(o), ref, "scale=%g %r" % (scale, seqlens), elementwise=False)
 
 
-def test_peaked_scores_full():
+@pytest.mark.parametrize("seqlens", [[1500, 700], [1560, 280]])
+def test_peaked_scores_full(seqlens):
     # scores 8x larger than N(0,1) inputs give: softmax rows dominated by a few keys, and the
     # running max moves often (exercises the rescale path)
-    seqlens = [1500, 700]
     w, q, k, v = draw(seqlens, 2, 128, seed=44, scale_q=8.0)
-    say("peaked")
+    say("peaked", seqlens)
     ref = oracle_full(q, k, v, seqlens, w.scale)
     o = run_varlen(q, k, v, seqlens)
-    assert_rows(as_f64(o), ref, "peaked", elementwise=False)
+    assert_rows(as_f64(o), ref, "peaked %r" % seqlens, elementwise=False)
 
 
-def test_increasing_scores_force_rescale():
+@pytest.mark.parametrize("L", [1024, 1044])
+def test_increasing_scores_force_rescale(L):
     # K rows grow along the sequence, so every tile raises the row max (by about 6 log2 units)
     # and every seventh or so passes the 2^40 headroom of the lazy maximum: the slow path then
     # rescales O and l in the middle of the sequence, several times
-    L, H, d = 1024, 1, 128
+    H, d = 1, 128
     g = torch.Generator().manual_seed(3)
     q = torch.ones((L, H, d)).to(torch.bfloat16)
     ramp = torch.linspace(0.0, 6.0, L).view(L, 1, 1)
     k = (ramp + 0.01 * torch.randn((L, H, d), generator=g)).to(torch.bfloat16)
     v = torch.randn((L, H, d), generator=g).to(torch.bfloat16)
     scale = W.Workload("x", (L,), H, d, 0).scale
-    say("forced rescale")
+    say("forced rescale", L)
     ref = oracle_full(q, k, v, [L], scale)
     o = run_varlen(q, k, v, [L])
-    assert_rows(as_f64(o), ref, "forced rescale", elementwise=False)
+    assert_rows(as_f64(o), ref, "forced rescale L=%d" % L, elementwise=False)
 
 
 
+@pytest.mark.parametrize("seqlens", [[640, 300], [536, 300]])
 @pytest.mark.parametrize("gap", [5.0, 38.0, 45.0, 200.0, 1000.0])
-def test_score_jump_mid_sequence(gap):
+def test_score_jump_mid_sequence(gap, seqlens):
     # One key in the middle of a segment (key 400, tile 6) scores `gap` log2 units above every
     # other key of every query row.  Below 40 the lazy maximum stays and the weights are up to
     # 2^gap times the earlier ones; above it the slow path must take the tile's maximum and
-    # rescale O and l (without it, gap >= 167 overflows the fp32 weights).
-    seqlens = [640, 300]
+    # rescale O and l (without it, gap >= 167 overflows the fp32 weights).  In the thin tile of
+    # the 536-query segment the key lies in the second 16-key block of its tile, so only the two
+    # waves holding that block see the jump and their maxima differ from the other six waves'.
     H, d = 2, 128
     g = torch.Generator().manual_seed(57)
     T = sum(seqlens)
@@ -231,12 +238,12 @@ def test_score_jump_mid_sequence(gap):
     c = float(np.float32(scale)) * 1.4426950408889634
     k[400, :, 0] = gap / (4.0 * c)
     q, k, v = q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
-    say("score jump", gap)
+    say("score jump", gap, seqlens)
     ref = oracle_full(q, k, v, seqlens, scale)
     o = run_varlen(q, k, v, seqlens)
     got = as_f64(o)
     assert np.all(np.isfinite(got))
-    assert_rows(got, ref, "score jump %g" % gap, elementwise=False)
+    assert_rows(got, ref, "score jump %g %r" % (gap, seqlens), elementwise=False)
 
 # ------------------------------------------------------------------------- full-size workloads
 
