@@ -103,7 +103,10 @@ int ts_attn_fwd(const void* q, const void* k, const void* v, void* o, int32_t B,
  * Work scheduling: a small planning kernel orders the segments longest first and the
  * attention kernel walks that order, so uneven batches finish with a short tail.  The plan
  * lives in a stream-ordered device allocation made and released by the call itself
- * (TS_ERR_NOMEM if it cannot be made).
+ * (TS_ERR_NOMEM if it cannot be made).  A batch of one segment (nseq = 1) needs neither
+ * outside validation mode: the attention kernel checks its offsets against {0, T} itself (a
+ * mismatch is the same device-side no-op), and a total above max_seqlen returns TS_OK
+ * without device work.
  */
 int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
                        const int32_t* cu_seqlens, int32_t nseq, int32_t max_seqlen,
@@ -139,8 +142,10 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
  * o must not overlap q, k or v, and lse must not overlap any of q, k, v, o (TS_ERR_ALIAS).
  * Device memory: the plan and, for n > 1, float32 partial results (n * total_q * H * (d + 1)
  * floats) come from a stream-ordered pool allocation made and released by the call
- * (TS_ERR_NOMEM if it cannot be made).  Bad offsets behave as in ts_attn_fwd_varlen (a device
- * no-op, or TS_ERR_SEGMENTS under TS_ATTN_VALIDATE=1).  num_splits outside 0..16 and the size
+ * (TS_ERR_NOMEM if it cannot be made); a call of one segment needs no plan, and unsplit no
+ * allocation at all (as in ts_attn_fwd_varlen, against {0, total_q} and {0, total_k}).  Bad
+ * offsets behave as in ts_attn_fwd_varlen (a device no-op, or TS_ERR_SEGMENTS under
+ * TS_ATTN_VALIDATE=1).  num_splits outside 0..16 and the size
  * limits above (for max_seqlen_q and max_seqlen_k each) give TS_ERR_SHAPE.
  */
 int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, float* lse,

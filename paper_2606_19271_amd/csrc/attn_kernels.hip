@@ -1037,24 +1037,42 @@ attn_dense_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
 // plan layout (int32): [0] item count, [1] error flag, then per rank r (most keys first):
 // [2 + 2r] segment index, [3 + 2r] first item of that segment.  The items of a segment are
 // ordered head-major, then split, then query tile, so consecutive items share K/V ranges.
+// plan = null: a batch of one segment, run without a planning kernel.  Its only valid offsets
+// are {0, total_q} and {0, total_k}; every workgroup checks them and the call is a no-op
+// otherwise, as with a rejected plan.
+__device__ __forceinline__ bool one_segment_valid(const int32_t* __restrict__ cu_q,
+                                                  const int32_t* __restrict__ cu_k, int total_q,
+                                                  int total_k) {
+  return cu_q[0] == 0 && cu_q[1] == total_q && cu_k[0] == 0 && cu_k[1] == total_k;
+}
+
 template <int D, int kMode>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_varlen_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                    const __bf16* __restrict__ v, Out out, const int32_t* __restrict__ cu_q,
                    const int32_t* __restrict__ cu_k, const int32_t* __restrict__ plan, int nseq,
-                   int H, int n_split, int chunk, float c, int negate_q) {
+                   int H, int n_split, int chunk, float c, int negate_q, int total_q,
+                   int total_k) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int total = plan[0];
-  if ((int)blockIdx.x >= total) return;
-  const int item = remap_block(blockIdx.x, total, chunk);
-  // last rank whose first item is <= item (empty segments share starts with the next rank)
-  int lo = 0, hi = nseq;  // plan[3 + 2*lo] <= item < plan[3 + 2*hi] (with hi = nseq as +inf)
-  while (hi - lo > 1) {
-    int mid = (lo + hi) >> 1;
-    if (plan[3 + 2 * mid] <= item) lo = mid; else hi = mid;
+  int s = 0, local;
+  if (plan == nullptr) {
+    if (!one_segment_valid(cu_q, cu_k, total_q, total_k)) return;
+    const int total = H * n_split * ((total_q + kBM - 1) / kBM);
+    if ((int)blockIdx.x >= total) return;
+    local = remap_block(blockIdx.x, total, chunk);
+  } else {
+    const int total = plan[0];
+    if ((int)blockIdx.x >= total) return;
+    const int item = remap_block(blockIdx.x, total, chunk);
+    // last rank whose first item is <= item (empty segments share starts with the next rank)
+    int lo = 0, hi = nseq;  // plan[3 + 2*lo] <= item < plan[3 + 2*hi] (with hi = nseq as +inf)
+    while (hi - lo > 1) {
+      int mid = (lo + hi) >> 1;
+      if (plan[3 + 2 * mid] <= item) lo = mid; else hi = mid;
+    }
+    s = plan[2 + 2 * lo];
+    local = item - plan[3 + 2 * lo];
   }
-  const int s = plan[2 + 2 * lo];
-  const int local = item - plan[3 + 2 * lo];
   Item it;
   it.q_start = cu_q[s];
   it.q_len = cu_q[s + 1] - cu_q[s];
@@ -1081,12 +1099,15 @@ template <int D>
 __global__ void __launch_bounds__(kMergeThreads)
 attn_merge_kernel(const float* __restrict__ part_o, const float* __restrict__ part_lse,
                   int n_split, int64_t rows, __bf16* __restrict__ o, float* __restrict__ lse,
-                  const int32_t* __restrict__ plan) {
+                  const int32_t* __restrict__ plan, const int32_t* __restrict__ cu_q,
+                  const int32_t* __restrict__ cu_k, int total_q, int total_k) {
   constexpr int kChunks = D / 8;
   const int64_t gid = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
   const int64_t row = gid / kChunks;
   const int c8 = (int)(gid % kChunks);
-  if (row >= rows || plan[1] != 0) return;  // a rejected plan wrote no partials: O stays as is
+  // rejected offsets wrote no partials: O stays as is
+  if (row >= rows) return;
+  if (plan != nullptr ? plan[1] != 0 : !one_segment_valid(cu_q, cu_k, total_q, total_k)) return;
   float m = -INFINITY;
   for (int i = 0; i < n_split; ++i) m = fmaxf(m, part_lse[i * rows + row]);
   f32x4 a0 = {0.0f, 0.0f, 0.0f, 0.0f}, a1 = a0;
@@ -1209,10 +1230,13 @@ static hipError_t launch_dense_d(const DenseArgs& a, hipStream_t st) {
 
 template <int D>
 static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a.cu_q, a.cu_k, a.nseq,
-                     a.max_q, a.max_k, a.total_q, a.total_k, a.H, a.n_split, a.plan);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e;
+  if (a.plan != nullptr) {
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, a.cu_q, a.cu_k, a.nseq,
+                       a.max_q, a.max_k, a.total_q, a.total_k, a.H, a.n_split, a.plan);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int64_t grid = packed_grid_bound(a.total_q, a.nseq, a.H, a.n_split);
   const float c = fabsf(a.scale) * kLog2e;
   const int neg = a.scale < 0.0f ? 1 : 0;
@@ -1221,19 +1245,21 @@ static hipError_t launch_packed_d(const PackedArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((attn_varlen_kernel<D, kFinal>), dim3((unsigned)grid), dim3(kThreads),
                        Geo<D>::kLds, st, (const __bf16*)a.q, (const __bf16*)a.k,
                        (const __bf16*)a.v, out, a.cu_q, a.cu_k, a.plan, a.nseq, a.H, 1,
-                       a.xcd_chunk, c, neg);
+                       a.xcd_chunk, c, neg, a.total_q, a.total_k);
     return hipGetLastError();
   }
   hipLaunchKernelGGL((attn_varlen_kernel<D, kPartial>), dim3((unsigned)grid), dim3(kThreads),
                      Geo<D>::kLds, st, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     out, a.cu_q, a.cu_k, a.plan, a.nseq, a.H, a.n_split, a.xcd_chunk, c, neg);
+                     out, a.cu_q, a.cu_k, a.plan, a.nseq, a.H, a.n_split, a.xcd_chunk, c, neg,
+                     a.total_q, a.total_k);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t rows = (int64_t)a.total_q * a.H;
   const int64_t threads = rows * (D / 8);
   const int64_t blocks = (threads + kMergeThreads - 1) / kMergeThreads;
   hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
-                     a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse, a.plan);
+                     a.part_o, a.part_lse, a.n_split, rows, (__bf16*)a.o, a.lse, a.plan, a.cu_q,
+                     a.cu_k, a.total_q, a.total_k);
   return hipGetLastError();
 }
 

@@ -31,7 +31,8 @@ struct PackedArgs {
   int32_t nseq, max_q, max_k, total_q, total_k, H, d, n_split;
   float scale;
   int xcd_chunk;
-  int32_t* plan;         // device, plan_ints(nseq) entries
+  int32_t* plan;         // device, plan_ints(nseq) entries; null for a batch of one segment
+                         // run without the planning kernel
   float* part_o;         // device [n_split][total_q][H][d] (n_split > 1)
   float* part_lse;       // device [n_split][total_q][H] (n_split > 1)
 };

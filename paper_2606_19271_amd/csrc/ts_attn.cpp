@@ -222,15 +222,34 @@ void carve(tsattn::PackedArgs& a, char* buf) {
 
 // Plan buffer (and split workspace) from the device's pool, the launches, the optional
 // validation read-back, and the stream-ordered release.
+// A batch of one segment runs without the planning kernel: its only valid offsets are {0, total_q}
+// and {0, total_k}, which the attention and merge kernels check themselves (a mismatch makes the
+// call a device-side no-op, as a rejected plan does).  Totals beyond the stated maximum lengths
+// admit no valid offsets at all, so such a call is a no-op without any device work.
+bool one_segment_possible(const tsattn::PackedArgs& a) {
+  return a.total_q <= a.max_q && a.total_k <= a.max_k;
+}
+
 int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
+  const bool validate = validate_mode();
+  // validation mode keeps the plan, whose error flag it reads back
+  const bool single = a.nseq == 1 && !validate;
+  if (single) {
+    if (!one_segment_possible(a)) return TS_OK;
+    if (a.n_split == 1) {  // no device memory at all
+      a.plan = nullptr;
+      return tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
+    }
+  }
   hipMemPool_t pool = device_pool(st);
   if (!pool) return TS_ERR_NOMEM;
   const size_t bytes = (size_t)scratch_bytes(a.nseq, a.n_split, a.total_q, a.H, a.d);
   char* buf = nullptr;
   if (hipMallocFromPoolAsync((void**)&buf, bytes, pool, s) != hipSuccess) return TS_ERR_NOMEM;
   carve(a, buf);
+  if (single) a.plan = nullptr;  // a split call of one segment: partials only
   int rc = tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
-  if (rc == TS_OK && validate_mode()) {
+  if (rc == TS_OK && validate) {
     int32_t head[2] = {0, 0};
     if (hipMemcpyAsync(head, a.plan, sizeof head, hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
@@ -379,6 +398,10 @@ int ts_attn_fwd_kvcache_noalloc(const void* q, const void* k, const void* v, voi
                        max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
   carve(a, (char*)st->scratch);
+  if (nseq == 1) {
+    if (!one_segment_possible(a)) return TS_OK;
+    a.plan = nullptr;
+  }
   return tsattn::launch_packed(a, (hipStream_t)stream) == hipSuccess ? TS_OK : TS_ERR_HIP;
 }
 

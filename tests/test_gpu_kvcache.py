@@ -233,6 +233,40 @@ def test_kv_rejected_offsets_leave_outputs_untouched():
         assert bool((o == 7.0).all()) and bool((lse == 123.0).all()), "splits=%d" % splits
 
 
+@pytest.mark.parametrize("splits", [1, 3])
+def test_kv_one_segment_bad_offsets_are_noops(splits):
+    # A call of one segment runs without the planning kernel: the attention and merge kernels
+    # check its offsets against {0, total} themselves.  Offsets that do not start at 0 or do not
+    # end at the tensors' rows leave O and lse untouched; so do totals beyond max_seqlen, which
+    # the host turns away before any device work; and validation mode still reports them.
+    w, q, k, v = draw([64], [128], 1, 64, 93)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    bad = [([0, 64], [0, 100], 64, 128), ([0, 64], [28, 128], 64, 128), ([5, 64], [0, 128], 64, 128),
+           ([0, 64], [0, 128], 32, 128), ([0, 64], [0, 128], 64, 100)]
+    for cq_l, ck_l, max_q, max_k in bad:
+        o = torch.full((64, 1, 64), 7.0, dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((64, 1), 123.0, dtype=torch.float32, device="cuda")
+        what = "one segment cu_q=%r cu_k=%r max=%d,%d splits=%d" % (cq_l, ck_l, max_q, max_k, splits)
+        say(what)
+        cq = torch.tensor(cq_l, dtype=torch.int32, device="cuda")
+        ck = torch.tensor(ck_l, dtype=torch.int32, device="cuda")
+        ts.ts_attn_fwd_kvcache(qd, kd, vd, cq, ck, max_q, max_k, out=o, lse=lse, num_splits=splits)
+        torch.cuda.synchronize()
+        assert bool((o == 7.0).all()) and bool((lse == 123.0).all()), what
+        os.environ["TS_ATTN_VALIDATE"] = "1"
+        try:
+            with pytest.raises(ts.TsAttnError) as ei:
+                ts.ts_attn_fwd_kvcache(qd, kd, vd, cq, ck, max_q, max_k, out=o, num_splits=splits)
+            assert ei.value.status == 10, what
+        finally:
+            del os.environ["TS_ATTN_VALIDATE"]
+    # the same tensors with their true offsets give the oracle's result
+    o, l = run_kv(w, q, k, v, splits=splits)
+    ro, rl = oracle(w, q, k, v, w.scale)
+    assert_rows(as_f64(o), ro, "one segment splits=%d" % splits, elementwise=False)
+    check_lse(l, rl, "one segment splits=%d" % splits)
+
+
 def test_kv_offsets_that_wrap_int32_are_rejected():
     # key offsets whose wrapping differences pass a differences-only check (see the packed test)
     Tk, nseq, max_k = 1024, 512, (1 << 24) - 512

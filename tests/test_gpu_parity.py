@@ -370,11 +370,25 @@ def test_bad_cu_seqlens_is_a_noop_and_validate_mode_reports_it():
         cu = torch.tensor([0, 300], dtype=torch.int32, device="cuda")
         with pytest.raises(ts.TsAttnError):
             ts.ts_attn_fwd_varlen(q, q, q, cu, 100, out=o)
+        # one segment whose end is not the tensors' row count (checked by the attention kernel
+        # itself outside validation mode, below)
+        short = torch.tensor([0, 200], dtype=torch.int32, device="cuda")
+        with pytest.raises(ts.TsAttnError):
+            ts.ts_attn_fwd_varlen(q, q, q, short, 300, out=o)
         # and a valid batch passes
         ts.ts_attn_fwd_varlen(q, q, q, cu, 300, out=o)
     finally:
         del os.environ["TS_ATTN_VALIDATE"]
     torch.cuda.synchronize()
+    # outside validation mode a batch of one segment runs without the planning kernel; bad
+    # offsets (not ending at the row count, or not starting at 0) or a total beyond max_seqlen
+    # still leave o untouched
+    for cu_l, max_len in (([0, 200], 300), ([100, 300], 300), ([0, 300], 100)):
+        o = torch.full((T, H, d), 7.0, dtype=torch.bfloat16, device="cuda")
+        ts.ts_attn_fwd_varlen(q, q, q, torch.tensor(cu_l, dtype=torch.int32, device="cuda"),
+                              max_len, out=o)
+        torch.cuda.synchronize()
+        assert bool((o == 7.0).all()), (cu_l, max_len)
 
 
 def wrapping_offsets(T, nseq, max_len):
