@@ -41,8 +41,9 @@
  *  - Graph capture: ts_attn_fwd only enqueues kernels, so a call on a capturing stream is
  *    recorded into the HIP graph and replays with the pointers and sizes it was made with.
  *    ts_attn_fwd_varlen, ts_attn_fwd_kvcache and ts_state_copy return TS_ERR_CAPTURE on a
- *    capturing stream: the first two take their plan buffer from a stream-ordered memory pool,
- *    and the copy looks up where its operands live.  So does any call that would be the first
+ *    capturing stream: the first two take their plan buffer from a library-owned device
+ *    workspace (ordered between calls by an event) or a stream-ordered memory pool, and the
+ *    copy looks up where its operands live.  So does any call that would be the first
  *    on its device, since the one-time device set-up must run outside capture.
  *    ts_attn_fwd_kvcache_noalloc allocates nothing and is not refused (after the device's
  *    first call).
@@ -102,11 +103,14 @@ int ts_attn_fwd(const void* q, const void* k, const void* v, void* o, int32_t B,
  * on stream and returns TS_ERR_SEGMENTS.
  * Work scheduling: a small planning kernel orders the segments longest first and the
  * attention kernel walks that order, so uneven batches finish with a short tail.  The plan
- * lives in a stream-ordered device allocation made and released by the call itself
- * (TS_ERR_NOMEM if it cannot be made).  A batch of one segment (nseq = 1) needs neither
- * outside validation mode: the attention kernel checks its offsets against {0, T} itself (a
- * mismatch is the same device-side no-op), and a total above max_seqlen returns TS_OK
- * without device work.
+ * lives in a device workspace the library keeps per device (grown when a call needs more, up to
+ * 256 MiB, and held until the process ends; TS_ERR_NOMEM if it cannot be grown).  The calls
+ * that use it take it in turn: each one's stream waits on the GPU for an event recorded after
+ * the previous one, so the host never waits, calls on one stream keep their order, and such
+ * calls on different streams run one after the other.  A batch of one segment (nseq = 1)
+ * needs no plan outside validation mode: the attention kernel checks its offsets against
+ * {0, T} itself (a mismatch is the same device-side no-op), and a total above max_seqlen
+ * returns TS_OK without device work.
  */
 int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
                        const int32_t* cu_seqlens, int32_t nseq, int32_t max_seqlen,
@@ -141,8 +145,10 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
  *                  the offsets coincide.
  * o must not overlap q, k or v, and lse must not overlap any of q, k, v, o (TS_ERR_ALIAS).
  * Device memory: the plan and, for n > 1, float32 partial results (n * total_q * H * (d + 1)
- * floats) come from a stream-ordered pool allocation made and released by the call
- * (TS_ERR_NOMEM if it cannot be made); a call of one segment needs no plan, and unsplit no
+ * floats) come from the workspace of ts_attn_fwd_varlen, or, when they exceed its 256 MiB,
+ * from a stream-ordered pool allocation made and released by the call (TS_ERR_NOMEM if it
+ * cannot be made; HIP's pool makes the host wait for the stream there); a call of one segment
+ * needs no plan, and unsplit no
  * allocation at all (as in ts_attn_fwd_varlen, against {0, total_q} and {0, total_k}).  Bad
  * offsets behave as in ts_attn_fwd_varlen (a device no-op, or TS_ERR_SEGMENTS under
  * TS_ATTN_VALIDATE=1).  num_splits outside 0..16 and the size

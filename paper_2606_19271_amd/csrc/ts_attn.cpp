@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -30,6 +31,13 @@ struct DeviceState {
   void* scratch = nullptr;          // this device's copy of the static scratch array
   std::once_flag pool_once;         // the pool is made by the first call that allocates
   hipMemPool_t pool = nullptr;      // null if its creation failed
+  // The workspace of the packed and chunk calls (see run_packed): grown when a call needs more,
+  // held until the process ends; `done` is recorded after each call that used it.
+  std::mutex ws_mu;
+  void* ws = nullptr;
+  size_t ws_size = 0;
+  hipEvent_t ws_done = nullptr;
+  bool ws_used = false;
 };
 
 DeviceState g_dev[kMaxDevices];
@@ -230,22 +238,9 @@ bool one_segment_possible(const tsattn::PackedArgs& a) {
   return a.total_q <= a.max_q && a.total_k <= a.max_k;
 }
 
-int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
-  const bool validate = validate_mode();
-  // validation mode keeps the plan, whose error flag it reads back
-  const bool single = a.nseq == 1 && !validate;
-  if (single) {
-    if (!one_segment_possible(a)) return TS_OK;
-    if (a.n_split == 1) {  // no device memory at all
-      a.plan = nullptr;
-      return tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
-    }
-  }
-  hipMemPool_t pool = device_pool(st);
-  if (!pool) return TS_ERR_NOMEM;
-  const size_t bytes = (size_t)scratch_bytes(a.nseq, a.n_split, a.total_q, a.H, a.d);
-  char* buf = nullptr;
-  if (hipMallocFromPoolAsync((void**)&buf, bytes, pool, s) != hipSuccess) return TS_ERR_NOMEM;
+// Launch of a packed call whose plan (and partials) sit in buf, and the validation-mode read-back
+// of the plan's error flag (a host synchronization, in validation mode only).
+int launch_with(tsattn::PackedArgs a, char* buf, bool single, bool validate, hipStream_t s) {
   carve(a, buf);
   if (single) a.plan = nullptr;  // a split call of one segment: partials only
   int rc = tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
@@ -257,6 +252,62 @@ int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
     else if (head[1] != 0)
       rc = TS_ERR_SEGMENTS;
   }
+  return rc;
+}
+
+// Workspaces up to this size come from the device's cached workspace; larger ones (long split
+// calls) from a stream-ordered pool allocation of their own.
+constexpr size_t kWorkspaceCache = (size_t)256 << 20;
+
+int run_packed(DeviceState* st, tsattn::PackedArgs a, hipStream_t s) {
+  const bool validate = validate_mode();
+  // validation mode keeps the plan, whose error flag it reads back
+  const bool single = a.nseq == 1 && !validate;
+  if (single) {
+    if (!one_segment_possible(a)) return TS_OK;
+    if (a.n_split == 1) {  // no device memory at all
+      a.plan = nullptr;
+      return tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
+    }
+  }
+  const size_t bytes = (size_t)scratch_bytes(a.nseq, a.n_split, a.total_q, a.H, a.d);
+  if (bytes <= kWorkspaceCache) {
+    // The device's cached workspace.  A stream-ordered allocation per call would be simpler, but
+    // HIP's hipMallocFromPoolAsync / hipFreeAsync pair makes the host wait for the stream (every
+    // call would block its thread until the GPU caught up).  Instead each call makes its stream
+    // wait, on the GPU, for the previous user's event, and records its own: calls on one stream
+    // stay in order and calls on different streams take the workspace one after the other.
+    std::lock_guard<std::mutex> lock(st->ws_mu);
+    if (!st->ws_done && hipEventCreateWithFlags(&st->ws_done, hipEventDisableTiming) != hipSuccess) {
+      st->ws_done = nullptr;
+      return TS_ERR_HIP;
+    }
+    if (st->ws_used && hipStreamWaitEvent(s, st->ws_done, 0) != hipSuccess) return TS_ERR_HIP;
+    if (st->ws_size < bytes) {  // grow: the old workspace is released once its last user is done
+      const size_t want = std::max(bytes, std::min(kWorkspaceCache, 2 * st->ws_size));
+      if (st->ws) {
+        if (hipEventSynchronize(st->ws_done) != hipSuccess || hipFree(st->ws) != hipSuccess)
+          return TS_ERR_HIP;
+        st->ws = nullptr;
+        st->ws_size = 0;
+      }
+      if (hipMalloc(&st->ws, want) != hipSuccess) {
+        (void)hipGetLastError();
+        st->ws = nullptr;
+        return TS_ERR_NOMEM;
+      }
+      st->ws_size = want;
+    }
+    int rc = launch_with(a, (char*)st->ws, single, validate, s);
+    if (hipEventRecord(st->ws_done, s) != hipSuccess && rc == TS_OK) rc = TS_ERR_HIP;
+    st->ws_used = true;
+    return rc;
+  }
+  hipMemPool_t pool = device_pool(st);
+  if (!pool) return TS_ERR_NOMEM;
+  char* buf = nullptr;
+  if (hipMallocFromPoolAsync((void**)&buf, bytes, pool, s) != hipSuccess) return TS_ERR_NOMEM;
+  int rc = launch_with(a, buf, single, validate, s);
   if (hipFreeAsync(buf, s) != hipSuccess && rc == TS_OK) rc = TS_ERR_HIP;
   return rc;
 }
