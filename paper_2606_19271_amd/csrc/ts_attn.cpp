@@ -1,5 +1,5 @@
 // ts_attn.cpp -- the C ABI of libts_attn.so (declared in include/ts_attn.h): argument checks,
-// per-device set-up, the plan buffer of packed batches, and the launches.
+// per-device set-up, the workspace of packed batches, and the launches.
 #include "ts_attn.h"
 
 #include <hip/hip_runtime_api.h>
@@ -29,7 +29,7 @@ struct DeviceState {
   int xcd_chunk = 32;
   int cus = 256;
   void* scratch = nullptr;          // this device's copy of the static scratch array
-  std::once_flag pool_once;         // the pool is made by the first call that allocates
+  std::once_flag pool_once;         // the pool is made by the first call that needs it
   hipMemPool_t pool = nullptr;      // null if its creation failed
   // The workspace of the packed and chunk calls (see run_packed): grown when a call needs more,
   // held until the process ends; `done` is recorded after each call that used it.
@@ -63,8 +63,9 @@ void init_device(int dev, DeviceState* st) {
   st->status = TS_OK;
 }
 
-// The device's stream-ordered memory pool for the plan buffers of the allocating calls, created
-// on first use (never under capture: those calls refuse a capturing stream before this).
+// The device's stream-ordered memory pool for the workspaces of packed calls too large for the
+// cached workspace (see run_packed), created on first use (never under capture: those calls refuse
+// a capturing stream before this).
 hipMemPool_t device_pool(DeviceState* st) {
   std::call_once(st->pool_once, [st] {
     hipMemPoolProps props;
@@ -74,7 +75,7 @@ hipMemPool_t device_pool(DeviceState* st) {
     props.location.id = st->dev;
     hipMemPool_t pool = nullptr;
     if (hipMemPoolCreate(&pool, &props) != hipSuccess) { (void)hipGetLastError(); return; }
-    uint64_t keep = UINT64_MAX;  // keep freed plan buffers in the pool between calls
+    uint64_t keep = UINT64_MAX;  // keep freed workspaces in the pool between calls
     if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) {
       (void)hipGetLastError();
       (void)hipMemPoolDestroy(pool);
@@ -228,8 +229,6 @@ void carve(tsattn::PackedArgs& a, char* buf) {
   }
 }
 
-// Plan buffer (and split workspace) from the device's pool, the launches, the optional
-// validation read-back, and the stream-ordered release.
 // A batch of one segment runs without the planning kernel: its only valid offsets are {0, total_q}
 // and {0, total_k}, which the attention and merge kernels check themselves (a mismatch makes the
 // call a device-side no-op, as a rejected plan does).  Totals beyond the stated maximum lengths
@@ -398,7 +397,8 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
   if (rc != TS_OK) return rc;
   if (tsattn::packed_grid_bound(total_tokens, nseq, H, 1) >= kGridLimit) return TS_ERR_SHAPE;
   if (nseq == 0 || total_tokens == 0) return TS_OK;
-  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
+  // the workspace may be grown, and its event waits and records do not belong in a graph
+  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;
   DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   tsattn::PackedArgs a{q, k, v, o, nullptr, cu_seqlens, cu_seqlens, nseq, max_seqlen, max_seqlen,
@@ -416,7 +416,8 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                               max_seqlen_k, total_q, total_k, H, d, scale, num_splits);
   if (rc != TS_OK) return rc;
   if (nseq == 0 || total_q == 0) return TS_OK;
-  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;  // the plan buffer is allocated
+  // the workspace may be grown, and its event waits and records do not belong in a graph
+  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;
   DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
   const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H, d);
