@@ -25,9 +25,10 @@
  *  - scale: any finite float (0 is allowed: O becomes the segment mean of V).  Typical:
  *    1/sqrt(d) rounded to float.
  *  - stream: a hipStream_t passed as void* (NULL = the legacy default stream).  Calls are
- *    asynchronous: they enqueue work on stream and return without synchronizing.  Buffers
- *    must stay valid until that work completes.  Device faults surface at the caller's next
- *    synchronization.
+ *    asynchronous: they enqueue work on stream and return without synchronizing (exceptions:
+ *    validation mode, the rare growth of the packed calls' workspace, and split partials beyond
+ *    its 256 MiB, see ts_attn_fwd_varlen and ts_attn_fwd_kvcache).  Buffers must stay valid
+ *    until that work completes.  Device faults surface at the caller's next synchronization.
  *  - Ownership: the caller owns every buffer; the library keeps no pointer after returning.
  *  - Errors: argument checks run on the host before any HIP call and return a ts_status
  *    without touching the device.  Empty problems (B, L, T or nseq equal to 0) are no-ops
