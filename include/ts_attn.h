@@ -39,15 +39,15 @@
  *    in the arithmetic, fixed reduction order), and a row's result does not depend on the
  *    other segments of the batch.
  *  - Thread safety: all entry points may be called concurrently from several host threads.
- *  - Graph capture: ts_attn_fwd only enqueues kernels, so a call on a capturing stream is
- *    recorded into the HIP graph and replays with the pointers and sizes it was made with.
- *    ts_attn_fwd_varlen, ts_attn_fwd_kvcache and ts_state_copy return TS_ERR_CAPTURE on a
- *    capturing stream: the first two take their plan buffer from a library-owned device
- *    workspace (ordered between calls by an event) or a stream-ordered memory pool, and the
- *    copy looks up where its operands live.  So does any call that would be the first
- *    on its device, since the one-time device set-up must run outside capture.
- *    ts_attn_fwd_kvcache_noalloc allocates nothing and is not refused (after the device's
- *    first call).
+ *  - Graph capture: the attention calls only enqueue kernels on a capturing stream, so they are
+ *    recorded into the HIP graph and replay with the pointers and sizes they were made with.
+ *    On a capturing stream ts_attn_fwd_varlen and ts_attn_fwd_kvcache run as
+ *    ts_attn_fwd_kvcache_noalloc does, on its static scratch array and under its rules (the
+ *    split count it can hold, replays that overlap other calls on the device race), instead of
+ *    the library's workspace, whose event waits and growth do not belong in a graph.
+ *    ts_state_copy returns TS_ERR_CAPTURE on a capturing stream (it looks up where its operands
+ *    live), and so does any call that would be the first on its device, since the one-time
+ *    device set-up must run outside capture.
  *  - Size limits: (L or max_seqlen + 256) * H * d * 2 bytes must stay below 2^31, and the
  *    work items (H * ceil(L / 256) per sequence; H * (ceil(T / 256) + nseq) for packed
  *    batches; 16 * H * (ceil(total_q / 256) + nseq) for chunk-vs-cache calls) below 2^23.
@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 5
+#define TS_ATTN_ABI_VERSION 6
 
 typedef enum ts_status {
   TS_OK = 0,

@@ -349,6 +349,27 @@ int copy_operand(const void* p, int dev, const void** devp, bool* host) {
   return TS_ERR_MEMORY;
 }
 
+// A packed or chunk call on the device's static scratch array: the allocation-free entry point,
+// and the allocating ones on a capturing stream (where the workspace's event waits and growth, or
+// a pool allocation, have no place).  n = 0 takes the library's choice, lowered until its partial
+// results fit the scratch; a forced n that does not fit returns TS_ERR_SCRATCH.  Validation mode
+// does not apply: invalid offsets make the call a device-side no-op.
+int run_static(DeviceState* st, tsattn::PackedArgs a, int32_t n, hipStream_t s) {
+  if (n == 0) {
+    n = auto_splits(st->cus, a.total_q, a.max_k, a.H, a.d);
+    while (n > 1 && scratch_bytes(a.nseq, n, a.total_q, a.H, a.d) > tsattn::kScratchBytes) --n;
+  } else if (scratch_bytes(a.nseq, n, a.total_q, a.H, a.d) > tsattn::kScratchBytes) {
+    return TS_ERR_SCRATCH;
+  }
+  a.n_split = n;
+  carve(a, (char*)st->scratch);
+  if (a.nseq == 1) {
+    if (!one_segment_possible(a)) return TS_OK;
+    a.plan = nullptr;
+  }
+  return tsattn::launch_packed(a, s) == hipSuccess ? TS_OK : TS_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -397,13 +418,12 @@ int ts_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o,
   if (rc != TS_OK) return rc;
   if (tsattn::packed_grid_bound(total_tokens, nseq, H, 1) >= kGridLimit) return TS_ERR_SHAPE;
   if (nseq == 0 || total_tokens == 0) return TS_OK;
-  // the workspace may be grown, and its event waits and records do not belong in a graph
-  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;
-  DeviceState* st = current_device(&rc, (hipStream_t)stream);
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);  // TS_ERR_CAPTURE for a first call
   if (!st) return rc;
   tsattn::PackedArgs a{q, k, v, o, nullptr, cu_seqlens, cu_seqlens, nseq, max_seqlen, max_seqlen,
                        total_tokens, total_tokens, H, d, 1, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
+  if (capturing((hipStream_t)stream)) return run_static(st, a, 1, (hipStream_t)stream);
   return run_packed(st, a, (hipStream_t)stream);
 }
 
@@ -416,14 +436,13 @@ int ts_attn_fwd_kvcache(const void* q, const void* k, const void* v, void* o, fl
                               max_seqlen_k, total_q, total_k, H, d, scale, num_splits);
   if (rc != TS_OK) return rc;
   if (nseq == 0 || total_q == 0) return TS_OK;
-  // the workspace may be grown, and its event waits and records do not belong in a graph
-  if (capturing((hipStream_t)stream)) return TS_ERR_CAPTURE;
-  DeviceState* st = current_device(&rc, (hipStream_t)stream);
+  DeviceState* st = current_device(&rc, (hipStream_t)stream);  // TS_ERR_CAPTURE for a first call
   if (!st) return rc;
-  const int32_t n = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H, d);
   tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
-                       max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
+                       max_seqlen_k, total_q, total_k, H, d, 1, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
+  if (capturing((hipStream_t)stream)) return run_static(st, a, num_splits, (hipStream_t)stream);
+  a.n_split = num_splits > 0 ? num_splits : auto_splits(st->cus, total_q, max_seqlen_k, H, d);
   return run_packed(st, a, (hipStream_t)stream);
 }
 
@@ -441,20 +460,10 @@ int ts_attn_fwd_kvcache_noalloc(const void* q, const void* k, const void* v, voi
     return TS_ERR_SCRATCH;
   DeviceState* st = current_device(&rc, (hipStream_t)stream);
   if (!st) return rc;
-  int32_t n = num_splits;
-  if (n == 0) {  // the library's choice, lowered until its partial results fit the scratch
-    n = auto_splits(st->cus, total_q, max_seqlen_k, H, d);
-    while (n > 1 && scratch_bytes(nseq, n, total_q, H, d) > tsattn::kScratchBytes) --n;
-  }
   tsattn::PackedArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, nseq, max_seqlen_q,
-                       max_seqlen_k, total_q, total_k, H, d, n, scale, st->xcd_chunk,
+                       max_seqlen_k, total_q, total_k, H, d, 1, scale, st->xcd_chunk,
                        nullptr, nullptr, nullptr};
-  carve(a, (char*)st->scratch);
-  if (nseq == 1) {
-    if (!one_segment_possible(a)) return TS_OK;
-    a.plan = nullptr;
-  }
-  return tsattn::launch_packed(a, (hipStream_t)stream) == hipSuccess ? TS_OK : TS_ERR_HIP;
+  return run_static(st, a, num_splits, (hipStream_t)stream);
 }
 
 int ts_state_copy(const void* src, int64_t src_bytes, void* dst, int64_t dst_bytes,
