@@ -12,6 +12,8 @@ Prints one JSON line:
                 workload, in the same unit; the sampled rows also serve as a parity check
   config.gemm_bf16_reference  context: torch.matmul's bf16 rate on a 16384^3 product, same device
                 and run (the sustainable MFMA rate at this device's power cap), and value over it
+  config.sdpa_flash_reference  context, dense workloads: torch's flash scaled_dot_product_attention
+                on the same inputs, same device and run, and value over it
 Other workloads (--workload): the dense and packed self-attention cases of workloads.WORKLOADS,
 and the chunk-vs-cache cases of workloads.KV_WORKLOADS (ts_attn_fwd_kvcache with the library's
 automatic key splits: flops = sum_s 4 Lq_s Lk_s d H; the events bracket the whole call, i.e. the
@@ -148,6 +150,32 @@ def gemm_reference(torch, dev, n=16384, reps=4):
     ms = e0.elapsed_time(e1) / reps
     del a, b, c
     return {"n": n, "ms": ms, "tflops": 2.0 * n ** 3 / (ms * 1e-3) / 1e12}
+
+
+def sdpa_reference(torch, qd, kd, vd, w, reps=5):
+    """Context only: torch's scaled_dot_product_attention on the same dense workload, same device
+    and run, restricted to its flash backend (so it never drops to the unfused math path); its
+    [B, H, L, d] operands are contiguous copies of the [T, H, d] inputs.  Returns the backend's
+    time and rate, or why it could not run."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    try:
+        q, k, v = (x.view(1, w.T, w.H, w.d).transpose(1, 2).contiguous() for x in (qd, kd, vd))
+        with sdpa_kernel(SDPBackend.FLASH_ATTENTION):
+            o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=w.scale)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=w.scale)
+            e1.record()
+            torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        del q, k, v, o
+        torch.cuda.empty_cache()
+        return {"backend": "flash", "ms": ms, "tflops": w.flops / (ms * 1e-3) / 1e12}
+    except Exception as e:  # noqa: BLE001 -- a missing backend is reported, not fatal
+        torch.cuda.empty_cache()
+        return {"unavailable": str(e).splitlines()[0][:200] if str(e) else type(e).__name__}
 
 
 PCIE5_X16_GBS = 64.0  # one direction, 32 GT/s x 16 lanes
@@ -325,6 +353,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm-reference", action="store_true",
                     help="skip the context timing of a plain bf16 matrix product")
+    ap.add_argument("--no-sdpa-reference", action="store_true",
+                    help="skip the context timing of torch's flash attention (dense workloads)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of attention, time a plain device copy of this many bytes "
                          "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known traffic)")
@@ -406,6 +436,7 @@ def main():
     achieved = w.flops / (kernel_ms * 1e-3) / 1e12
     traffic = traffic_bytes(w.name)
     gemm = None if args.no_gemm_reference else gemm_reference(torch, dev)
+    sdpa = None if args.no_sdpa_reference or not dense else sdpa_reference(torch, qd, kd, vd, w)
 
     result = {
         "metric": METRIC,
@@ -432,7 +463,10 @@ def main():
                    # kernel source (null when they were taken on another source), over the launch
                    "hbm_GBps_rocprof": None if traffic is None else traffic / (kernel_ms * 1e-3) / 1e9,
                    **({"gemm_bf16_reference": gemm,
-                       "value_over_gemm": value / gemm["tflops"]} if gemm else {})},
+                       "value_over_gemm": value / gemm["tflops"]} if gemm else {}),
+                   **({"sdpa_flash_reference": sdpa,
+                       "value_over_sdpa": value / sdpa["tflops"] if "tflops" in sdpa else None}
+                      if sdpa else {})},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic},
     }
