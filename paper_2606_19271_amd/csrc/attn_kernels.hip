@@ -96,6 +96,11 @@ struct Geo {
   static constexpr int kKDmaMax = (kKDma + kGroupWaves - 1) / kGroupWaves;  // per wave, at most
   static constexpr int kKDmaMin = kKDma / kGroupWaves;                      // per wave, at least
   static constexpr int kVDmaPerWave = kVDma / kGroupWaves;
+  // Pair steps of the softmax's exp work (16 per tile at d = 128, 32 at d = 64) between two of
+  // the vector step's DMA instructions.  Issued back to back, the four vector-step waves of a CU
+  // queue 16 KiB at once on its 64 B/clk address path, and each wave's exp work waits behind
+  // its own share of that queue.
+  static constexpr int kDmaEvery = 4;
   static_assert(kKTile % 1024 == 0 && kVTile % 1024 == 0 && kVDma % kGroupWaves == 0, "DMA split");
   static_assert(kVStages * kVTile <= 65536, "V addresses must fit the DS immediate");
   __host__ __device__ static constexpr int vswz(int r) {
@@ -293,18 +298,40 @@ __device__ __forceinline__ void pv_tile(const lds_char* __restrict__ vt, const V
     }
 }
 
+// Nothing to issue (see exp_pack).
+struct NoIssue {
+  __device__ void operator()(int) const {}
+};
+
 // exp2(S*c - m_c) for the 32 scores of the lane, packed to the bf16 B operands of the PV
 // product.  Returns the bitwise OR of the packed words: bit 14 of a bf16 is the top bit of its
 // exponent, set exactly when the (non-negative) value is at least 2 or not finite, so
 // (OR & 0x40004000) != 0 flags a tile whose weights are not all below 2.
-template <int NT, bool kMasked>
+// issue(0 .. kIssue - 1) is called in order, instruction i at the start of pair step
+// i * kEvery (kEvery = 0: all at the start): the vector step's K/V DMA instructions go there.
+template <int NT, bool kMasked, int kIssue = 0, int kEvery = 0, typename Issue = NoIssue>
 __device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[NT / 2], bf16x8 (&p)[NT],
-                                             float m_c, float c, int keys_valid, int hb) {
+                                             float m_c, float c, int keys_valid, int hb,
+                                             Issue&& issue = Issue{}) {
+  static_assert(kEvery * (kIssue - 1) < NT * 4, "issue points");
   unsigned any = 0;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
 #pragma unroll
     for (int m = 0; m < 8; m += 2) {
+      const int step = 4 * t + m / 2;
+      if (kIssue > 0 && (kEvery == 0 ? step == 0 : step % kEvery == 0 && step / kEvery < kIssue)) {
+        // the scheduling barriers keep the scheduler from gathering the memory instructions at
+        // the top again
+        __builtin_amdgcn_sched_barrier(0);
+        if (kEvery == 0) {
+#pragma unroll
+          for (int i = 0; i < kIssue; ++i) issue(i);
+        } else {
+          issue(step / (kEvery > 0 ? kEvery : 1));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
       float x0 = s[t >> 1][8 * (t & 1) + m], x1 = s[t >> 1][8 * (t & 1) + m + 1];
       float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x0, c, -m_c));
       float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x1, c, -m_c));
@@ -339,16 +366,23 @@ __device__ __forceinline__ unsigned exp_pack(const f32x16 (&s)[NT / 2], bf16x8 (
 // that here, in the rare slow path of the vector step, keeps the matrix step free of branches.
 constexpr float kBias = 39.0f;
 
-template <int D, bool kMasked>
+// issue(0 .. kIssue - 1): instructions to spread over the tile's exp work (see exp_pack); all
+// of them are issued once, on every path.
+template <int D, bool kMasked, int kIssue, typename Issue>
 __device__ __forceinline__ void softmax_tile(f32x16 (&s)[Geo<D>::kBN / 32],
                                              bf16x8 (&p)[Geo<D>::kBN / 16], float& m_c,
                                              f32x16 (&o)[D / 32], f32x4 (&l)[2], float c,
-                                             int keys_valid, int lane) {
+                                             int keys_valid, int lane, Issue&& issue) {
   constexpr int kBN = Geo<D>::kBN;
   const int hb = lane >> 5;
   if (!kMasked) {
-    const unsigned any = exp_pack<kBN / 16, false>(s, p, m_c, c, kBN, hb);
+    const unsigned any =
+        exp_pack<kBN / 16, false, kIssue, Geo<D>::kDmaEvery>(s, p, m_c, c, kBN, hb, issue);
     if (__builtin_amdgcn_ballot_w64((any & 0x40004000u) != 0) == 0) return;
+  }
+  if (kMasked) {
+#pragma unroll
+    for (int i = 0; i < kIssue; ++i) issue(i);
   }
   if (kMasked) {
 #pragma unroll
@@ -408,19 +442,28 @@ __device__ __forceinline__ void dma_offsets_v(int gw, int lane, int row_bytes,
 }
 
 // This wave's share of the DMA of the K tile whose first key is key0 (rows past the segment
-// end read as zeros through the descriptor's range check).
-template <int D>
+// end read as zeros through the descriptor's range check).  kFrom skips the first kFrom
+// instructions (issued one by one with dma_k_one).
+template <int D, int kFrom = 0>
 __device__ __forceinline__ void dma_k(__amdgpu_buffer_rsrc_t rk, int key0, int row_bytes,
                                       lds_char* tile, const int* koff, int gw) {
   using G = Geo<D>;
   const int skip = key0 * row_bytes;
 #pragma unroll
-  for (int u = 0; u < G::kKDmaMax; ++u) {
+  for (int u = kFrom; u < G::kKDmaMax; ++u) {
     const int n = gw + G::kGroupWaves * u;
     if (u < G::kKDmaMin || n < G::kKDma)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(tile + 1024 * n), 16, koff[u] + skip,
                                                0, 0, 0);
   }
+}
+// Instruction u < kKDmaMin of that share (every wave issues these, without a branch).
+template <int D>
+__device__ __forceinline__ void dma_k_one(__amdgpu_buffer_rsrc_t rk, int key0, int row_bytes,
+                                          lds_char* tile, const int* koff, int gw, int u) {
+  using G = Geo<D>;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(tile + 1024 * (gw + G::kGroupWaves * u)),
+                                           16, koff[u] + key0 * row_bytes, 0, 0, 0);
 }
 template <int D>
 __device__ __forceinline__ void dma_v(__amdgpu_buffer_rsrc_t rv, int key0, int row_bytes,
@@ -431,6 +474,13 @@ __device__ __forceinline__ void dma_v(__amdgpu_buffer_rsrc_t rv, int key0, int r
   for (int u = 0; u < G::kVDmaPerWave; ++u)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(tile + 1024 * (gw + G::kGroupWaves * u)),
                                              16, voff[u] + skip, 0, 0, 0);
+}
+template <int D>
+__device__ __forceinline__ void dma_v_one(__amdgpu_buffer_rsrc_t rv, int key0, int row_bytes,
+                                          lds_char* tile, const int* voff, int gw, int u) {
+  using G = Geo<D>;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(tile + 1024 * (gw + G::kGroupWaves * u)),
+                                           16, voff[u] + key0 * row_bytes, 0, 0, 0);
 }
 
 // Waits until at most N of this wave's vector-memory operations are outstanding.
@@ -558,6 +608,20 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
     if (!kGroupB) dma_k<D>(rk, key0, row_bytes, ktile(j & 3), koff, gw);
     else dma_v<D>(rv, key0, row_bytes, vtile(vstage), voff, gw);
   };
+  // The same fetch in two parts, for the vector steps: each of the kSpread instructions that
+  // every wave issues (without a branch) on its own, to be spread over the softmax, and then
+  // the one more K instruction of some waves of group A.
+  static_assert(G::kKDmaMin == G::kVDmaPerWave, "one spread for both fetching groups");
+  constexpr int kSpread = G::kVDmaPerWave;
+  auto fetch_one = [&](int j, int vstage, int u) {
+    const int key0 = min(it.tile_begin + j, seg_tiles) * kBN;
+    if (!kGroupB) dma_k_one<D>(rk, key0, row_bytes, ktile(j & 3), koff, gw, u);
+    else dma_v_one<D>(rv, key0, row_bytes, vtile(vstage), voff, gw, u);
+  };
+  auto fetch_rest = [&](int j) {
+    const int key0 = min(it.tile_begin + j, seg_tiles) * kBN;
+    if (!kGroupB) dma_k<D, kSpread>(rk, key0, row_bytes, ktile(j & 3), koff, gw);
+  };
   constexpr int kFetchAhead = kGroupB ? 2 : 3;  // tiles between a fetch and its first reader
   constexpr int kFetchWait = kGroupB ? G::kVDmaPerWave : G::kKDmaMin;  // fewest per wave
 
@@ -586,21 +650,23 @@ __device__ __forceinline__ void run_item_group(const Item& it, const __bf16* __r
   const int ntiles = it.ntiles;
   // valid keys of the item's last tile: fewer than kBN only on the segment's ragged last tile
   const int last_keys = min(kBN, it.k_len - (it.tile_begin + ntiles - 1) * kBN);
-  // vector step j: fetch tile j + kFetchAhead (a V tile into stage vst2 = (j + 2) % 3), softmax
-  // S_j -> P_j, wait for the fetch of the previous vector step, read the first K fragments of
+  // vector step j: fetch tile j + kFetchAhead (a V tile into stage vst2 = (j + 2) % 3), its
+  // instructions spread over the softmax S_j -> P_j, wait for the fetch of the previous vector
+  // step, read the first K fragments of
   // M(j + 1); kMasked on the last tile only, which has no M(j + 1) S product.  The barrier that
   // closes the step opens the next iteration, so the loop's branch is taken before it and the
   // matrix step that follows the barrier starts with its first MFMA.
   auto vstep = [&](int j, int vst2, auto masked) {
     constexpr bool kMasked = decltype(masked)::value;
-    fetch(j + kFetchAhead, vst2);
-    if constexpr (kActive)
-      softmax_tile<D, kMasked>(s, p, m_c, oacc, lacc, c, kMasked ? last_keys : kBN, lane);
+    auto issue = [&](int u) { fetch_one(j + kFetchAhead, vst2, u); };
+    if constexpr (kActive) {
+      softmax_tile<D, kMasked, kSpread>(s, p, m_c, oacc, lacc, c, kMasked ? last_keys : kBN, lane,
+                                        issue);
+    } else {
 #pragma unroll
-    for (int i = 0; i < G::kKDmaMax; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 3);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 3);
+      for (int u = 0; u < kSpread; ++u) issue(u);
     }
+    fetch_rest(j + kFetchAhead);
     wait_vmem<kFetchWait>();
     if (kActive && !kMasked) k_preread<D>(ktile((j + 1) & 3), kp, lane);
   };
